@@ -1,0 +1,68 @@
+"""Oracle: importance score, high-precision budget and top-k selection.
+
+Test infrastructure only.
+
+Importance (H2O policy, cited in Sections 3.1 and 4.1; Fig. 3 right): the
+paper adopts heavy-hitter accumulated attention without restating it.
+Reading: each decode step adds the step's post-softmax probability of every
+token to that token's score; no decay; a new token starts at 0; under
+grouped-query attention the probabilities of the query heads sharing a KV
+head are summed, left to right in query-head order, in fp32, and that sum is
+added to the score with one fp32 add.
+
+Selection (Fig. 3 right; Sections 2.1 and 3.1): tokens local to the current
+position (the recent window) and the top tokens by importance form the
+importance (high-precision) cache, every other token the retained
+(low-precision) cache.  Readings:
+  * the window is the last W positions and is always high precision;
+  * eligible tokens are those currently high precision and outside the window
+    (at the first selection after prefill: every token outside the window);
+  * the k_heavy eligible tokens with the largest key (score, position) are
+    kept -- a tie in score goes to the newer token -- and the other eligible
+    tokens are demoted;
+  * demotion is one way: a retained token is never promoted again (its
+    high-precision data no longer exists).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def heavy_budget(length: int, ratio_num: int, ratio_den: int, window: int, window_in_ratio: bool) -> int:
+    """Number of non-window tokens kept at high precision for a cache of
+    ``length`` tokens: floor(ratio * length), minus the window when the window
+    counts towards the ratio, and never below zero."""
+    k = (ratio_num * length) // ratio_den
+    if window_in_ratio:
+        k -= window
+    return max(0, k)
+
+
+def accumulate(acc, probs) -> np.ndarray:
+    """acc fp32 [L]; probs fp32 [G, L] -> acc + ((p_0 + p_1) + ...) in fp32."""
+    probs = np.asarray(probs, dtype=np.float32)
+    s = probs[0].copy()
+    for i in range(1, probs.shape[0]):
+        s = s + probs[i]
+    return np.asarray(acc, dtype=np.float32) + s
+
+
+def select(acc, is_hi, length: int, k_heavy: int, window: int, initial: bool) -> np.ndarray:
+    """Return the new high-precision mask [length] (bool).
+
+    acc fp32 [length]; is_hi bool [length] (ignored when ``initial``).
+    """
+    acc = np.asarray(acc, dtype=np.float32)[:length]
+    pos = np.arange(length)
+    in_window = pos >= length - window
+    if initial:
+        eligible = ~in_window
+    else:
+        eligible = np.asarray(is_hi, dtype=bool)[:length] & ~in_window
+    idx = pos[eligible]
+    # Sort by score descending, then position descending.
+    order = np.lexsort((-idx, -acc[idx]))
+    keep = idx[order[:k_heavy]]
+    new_hi = in_window.copy()
+    new_hi[keep] = True
+    return new_hi

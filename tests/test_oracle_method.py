@@ -1,0 +1,254 @@
+"""Pins for the oracle's balancer, attention, importance score, selection and
+decode step: closed forms, textbook special cases (torch's fp64 scaled dot
+product attention, a pure-Python softmax), brute force on tiny inputs and the
+invariants the paper states."""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2402_18096_amd import workloads
+
+SCALE = 1.0 / math.sqrt(128.0)
+
+
+# -- balancer (Eq. 2-4) -------------------------------------------------------
+
+def test_balancer_closed_form():
+    q = np.zeros((1, 3, 3), np.float16)   # G=1, T=3, D=3
+    k = np.zeros((3, 3), np.float16)
+    q[0, 1] = [4, -1, 0.25]
+    q[0, 2] = [-2, 0.5, 0.125]
+    k[0] = [1, -4, 16]
+    k[2] = [-0.5, 2, 8]
+    np.testing.assert_array_equal(oracle.balancer(q, k), np.array([2, 0.5, 0.125], np.float32))
+
+
+def test_balancer_group_max_and_zero_channels():
+    """Under GQA the query max runs over every head of the group; a channel
+    whose query or key is all zero gets b = 1."""
+    q = np.zeros((2, 2, 4), np.float16)
+    k = np.ones((2, 4), np.float16)
+    q[0, 0] = [1, 0, 9, 0]
+    q[1, 1] = [0, 0, -16, 4]
+    k[:, 3] = 0
+    b = oracle.balancer(q, k)
+    np.testing.assert_array_equal(b, np.array([1, 1, 4, 1], np.float32))
+
+
+def test_balancer_cancels_in_logits():
+    """Eq. 3-4: (q / b) . (k * b) = q . k exactly for power-of-two b."""
+    rng = np.random.default_rng(0)
+    q = rng.standard_normal((3, 128)).astype(np.float16)
+    k = rng.standard_normal((50, 128)).astype(np.float16)
+    v = rng.standard_normal((50, 128)).astype(np.float32)
+    b = (2.0 ** rng.integers(-3, 4, 128)).astype(np.float32)
+    o0, p0 = oracle.attention(q, k.astype(np.float32), v, SCALE)
+    o1, p1 = oracle.attention(q, oracle.balance_keys(k, b), v, SCALE, b)
+    np.testing.assert_array_equal(o0, o1)
+    np.testing.assert_array_equal(p0, p1)
+
+
+def test_balancer_equalises_channel_ranges():
+    """After balancing, max|q_hat| and max|k_hat| agree per channel (both
+    become sqrt(max|q| * max|k|)), the point of Eq. 2."""
+    rng = np.random.default_rng(1)
+    q = (rng.standard_normal((2, 40, 128)) * np.where(np.arange(128) < 4, 20, 1)).astype(np.float16)
+    k = (rng.standard_normal((40, 128)) * np.where(np.arange(128) % 7 == 0, 30, 1)).astype(np.float16)
+    b = oracle.balancer(q, k)
+    qm = np.abs(oracle.balance_query(q, b)).max(axis=(0, 1))
+    km = np.abs(oracle.balance_keys(k, b)).max(axis=0)
+    np.testing.assert_allclose(qm, km, rtol=1e-6)
+
+
+# -- attention ----------------------------------------------------------------
+
+def test_attention_matches_torch_sdpa_fp64():
+    rng = np.random.default_rng(2)
+    q = rng.standard_normal((4, 128)).astype(np.float16)
+    k = rng.standard_normal((300, 128)).astype(np.float32) * 3
+    v = rng.standard_normal((300, 128)).astype(np.float32)
+    o, p = oracle.attention(q, k, v, SCALE)
+    tq = torch.from_numpy(q.astype(np.float64))[None, :, None, :]
+    tk = torch.from_numpy(k.astype(np.float64))[None, None].expand(1, 4, 300, 128)
+    tv = torch.from_numpy(v.astype(np.float64))[None, None].expand(1, 4, 300, 128)
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, scale=SCALE)[0, :, 0].numpy()
+    np.testing.assert_allclose(o, ref, rtol=1e-6, atol=1e-7)
+
+
+def test_attention_pure_python_softmax():
+    rng = np.random.default_rng(3)
+    q = rng.standard_normal((2, 6)).astype(np.float16)
+    k = rng.standard_normal((5, 6)).astype(np.float32)
+    v = rng.standard_normal((5, 6)).astype(np.float32)
+    b = np.array([1, 2, 0.5, 3, 1, 0.25], np.float32)
+    o, p = oracle.attention(q, k, v, 0.3, b)
+    for i in range(2):
+        qh = [float(np.float32(np.float32(q[i, c]) / b[c])) for c in range(6)]
+        s = [0.3 * math.fsum(qh[c] * float(k[j, c]) for c in range(6)) for j in range(5)]
+        m = max(s)
+        e = [math.exp(x - m) for x in s]
+        z = math.fsum(e)
+        for j in range(5):
+            assert abs(p[i, j] - e[j] / z) <= 1e-7
+        for c in range(6):
+            assert abs(o[i, c] - math.fsum(e[j] / z * float(v[j, c]) for j in range(5))) <= 1e-6
+
+
+def test_attention_permutation_invariance():
+    """Section 3.4: permuting K/V pairs together permutes p and leaves o."""
+    rng = np.random.default_rng(4)
+    q = rng.standard_normal((2, 128)).astype(np.float16)
+    k = rng.standard_normal((200, 128)).astype(np.float32)
+    v = rng.standard_normal((200, 128)).astype(np.float32)
+    perm = rng.permutation(200)
+    o0, p0 = oracle.attention(q, k, v, SCALE)
+    o1, p1 = oracle.attention(q, k[perm], v[perm], SCALE)
+    np.testing.assert_allclose(o0, o1, rtol=1e-6, atol=1e-7)
+    np.testing.assert_allclose(p0[:, perm], p1, rtol=1e-6, atol=1e-12)
+
+
+# -- importance -----------------------------------------------------------------
+
+def test_accumulate_brute_force_order():
+    rng = np.random.default_rng(5)
+    acc = rng.random(40).astype(np.float32)
+    p = (rng.random((4, 40)) * 1e-3).astype(np.float32)
+    out = oracle.accumulate(acc, p)
+    for j in range(40):
+        s = np.float32(p[0, j])
+        for i in range(1, 4):
+            s = np.float32(s + p[i, j])
+        assert out[j] == np.float32(acc[j] + s)
+
+
+def test_accumulate_mass_grows_by_group_size():
+    """Every query's probabilities sum to 1, so the total score grows by G."""
+    rng = np.random.default_rng(6)
+    s = rng.standard_normal((4, 500))
+    p = (np.exp(s) / np.exp(s).sum(1, keepdims=True)).astype(np.float32)
+    acc = np.zeros(500, np.float32)
+    out = oracle.accumulate(acc, p)
+    assert abs(float(out.sum(dtype=np.float64)) - 4.0) < 1e-5
+
+
+# -- selection ------------------------------------------------------------------
+
+def test_select_worked_example():
+    acc = np.array([0.5, 0.25, 0.25, 0.125, 0.9], np.float32)
+    hi = oracle.select(acc, None, 5, 2, 1, initial=True)
+    assert np.nonzero(hi)[0].tolist() == [0, 2, 4]
+
+
+def test_select_brute_force_small():
+    """Against exhaustive search: the kept set is the k-subset of eligible
+    tokens whose sorted (score, position) keys are lexicographically largest."""
+    rng = np.random.default_rng(7)
+    for trial in range(200):
+        L = int(rng.integers(1, 9))
+        W = int(rng.integers(0, 3))
+        acc = rng.integers(0, 4, L).astype(np.float32) / 4    # many ties
+        is_hi = rng.random(L) < 0.7
+        initial = bool(trial % 2)
+        k = int(rng.integers(0, L + 1))
+        got = oracle.select(acc, is_hi, L, k, W, initial)
+        win = set(range(max(0, L - W), L))
+        elig = [j for j in range(L) if j not in win and (initial or is_hi[j])]
+        best = None
+        for sub in itertools.combinations(elig, min(k, len(elig))):
+            key = sorted(((acc[j], j) for j in sub), reverse=True)
+            if best is None or key > best[0]:
+                best = (key, set(sub))
+        expect = win | (best[1] if best else set())
+        assert set(np.nonzero(got)[0].tolist()) == expect, (L, W, k, acc, is_hi, initial)
+
+
+def test_select_invariants():
+    rng = np.random.default_rng(8)
+    L, W, k = 1000, 64, 136
+    acc = rng.random(L).astype(np.float32)
+    is_hi = rng.random(L) < 0.3
+    is_hi[-W:] = True
+    new = oracle.select(acc, is_hi, L, k, W, initial=False)
+    assert new[-W:].all()                        # window always high
+    assert not (new & ~is_hi).any()              # no promotion
+    assert new.sum() == W + min(k, int(is_hi[:-W].sum()))
+
+
+def test_heavy_budget():
+    assert oracle.heavy_budget(513, 1, 5, 32, False) == 102
+    assert oracle.heavy_budget(4097, 1, 4, 64, True) == 960
+    assert oracle.heavy_budget(32769, 1, 10, 128, True) == 3148
+    assert oracle.heavy_budget(100, 1, 10, 128, True) == 0
+
+
+# -- the decode step ------------------------------------------------------------
+
+def _tiny_inputs(wl, T, steps, seed=0):
+    wl = wl.with_(context=T, seed=seed)
+    k, v = workloads.prefill_kv(wl)
+    sc = workloads.initial_scores(wl)
+    q, kn, vn = workloads.decode_inputs(wl, steps)
+    H = wl.n_heads
+    rs = lambda x: x.reshape(H, *x.shape[2:]).numpy()
+    return wl, rs(k), rs(v), sc.reshape(H, -1).numpy(), q, kn, vn
+
+
+def test_all_high_fp16_equals_plain_attention():
+    """With every token kept fp16 the step is textbook attention over the
+    fp16-rounded keys and values (torch SDPA, fp64)."""
+    wl = workloads.WORKLOADS["tiny"].with_(batch=1, q_heads=2, kv_heads=2)
+    wl, k, v, sc, q, kn, vn = _tiny_inputs(wl, 40, 2)
+    c = oracle.OracleCache(wl.n_heads, 1, 64, 16, 2, 32)
+    c.prefill(k, v, sc, k_heavy=100, window=0)
+    for t in range(2):
+        o, p = c.step(q[t, 0][:, None].numpy(), kn[t, 0].numpy(), vn[t, 0].numpy(), SCALE, 100, 0)
+        K = np.concatenate([k, kn[: t + 1, 0].numpy().transpose(1, 0, 2)], axis=1).astype(np.float64)
+        V = np.concatenate([v, vn[: t + 1, 0].numpy().transpose(1, 0, 2)], axis=1).astype(np.float64)
+        tq = torch.from_numpy(q[t, 0].numpy().astype(np.float64))[None, :, None, :]
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            tq, torch.from_numpy(K)[None], torch.from_numpy(V)[None], scale=SCALE)[0, :, 0].numpy()
+        np.testing.assert_allclose(o[:, 0], ref, rtol=1e-6, atol=1e-6)
+
+
+def test_uniform_rtn_special_case():
+    """Ratio 0 and window 0: every token ends up in the retained cache, i.e.
+    uniform per-token RTN quantization of the whole cache (the RTN baseline)."""
+    wl = workloads.WORKLOADS["tiny"].with_(batch=1, q_heads=2, kv_heads=2)
+    wl, k, v, sc, q, kn, vn = _tiny_inputs(wl, 64, 1)
+    c = oracle.OracleCache(wl.n_heads, 1, 80, 16, 2, 32)
+    c.prefill(k, v, sc, k_heavy=0, window=0)
+    assert not c.is_hi[:, :64].any()
+    c.step(q[0, 0][:, None].numpy(), kn[0, 0].numpy(), vn[0, 0].numpy(), SCALE, 0, 0)
+    assert not c.is_hi[:, :65].any()
+    # the appended token went fp16 -> INT2 on demotion: codes are Eq. 1 of its fp16 value
+    codes, a, b = oracle.quantize(kn[0, 0].numpy().astype(np.float32), 2, 32)
+    np.testing.assert_array_equal(c.lk[:, 64], codes)
+    np.testing.assert_array_equal(c.lk_a[:, 64], a)
+
+
+def test_step_invariants_and_demotion_path():
+    wl = workloads.WORKLOADS["tiny"]
+    wl, k, v, sc, q, kn, vn = _tiny_inputs(wl, 200, 6, seed=3)
+    c = oracle.OracleCache(wl.n_heads, 1, 210, 8, 4, 64)
+    kh0 = oracle.heavy_budget(200, 1, 5, 16, False)
+    c.prefill(k, v, sc, kh0, 16)
+    assert (c.is_hi[:, :200].sum(1) == kh0 + 16).all()
+    for t in range(6):
+        before = c.is_hi.copy()
+        hk, hka, hkb = c.hk.copy(), c.hk_a.copy(), c.hk_b.copy()
+        L = 201 + t
+        kh = oracle.heavy_budget(L, 1, 5, 16, False)
+        c.step(q[t, 0][:, None].numpy(), kn[t, 0].numpy(), vn[t, 0].numpy(), SCALE, kh, 16)
+        assert (c.is_hi[:, :L].sum(1) == kh + 16).all()
+        assert c.is_hi[:, L - 16:L].all()
+        before[:, L - 1] = True
+        assert not (c.is_hi & ~before).any()
+        for h in range(wl.n_heads):
+            for j in np.nonzero(before[h, :L] & ~c.is_hi[h, :L])[0]:
+                val = oracle.dequantize(hk[h, j], hka[h, j], hkb[h, j], 64)
+                codes, a, b = oracle.quantize(val, 4, 64)
+                np.testing.assert_array_equal(c.lk[h, j], codes)
