@@ -1,0 +1,254 @@
+/*
+ * mikv.h -- C ABI of libmikv.so: the decode hot path of MiKV
+ * ("No Token Left Behind: Reliable KV Cache Compression via Importance-Aware
+ * Mixed Precision Quantization", arXiv 2402.18096) for AMD MI355X (gfx950).
+ *
+ * A MiKV cache keeps, per (sequence, KV head), the tokens ranked important
+ * by accumulated attention at high precision (fp16 or INT8: the "importance
+ * cache") and every other token at low precision (INT4/INT2, per-token
+ * grouped asymmetric: the "retained cache") instead of evicting it
+ * (Section 3, Fig. 3).  Because attention after RoPE is permutation
+ * invariant, the two precisions are stored as two separate pools (Section
+ * 3.4); a token's position travels with it in a position array.
+ *
+ * Conventions shared by every entry point
+ *  - All pointers named in a mikv_cache and every array argument are DEVICE
+ *    pointers unless stated otherwise.  The caller allocates everything; the
+ *    library allocates no memory and keeps no state between calls apart from
+ *    its loaded code objects.
+ *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream).  Results are valid once the stream has synchronised.  Calls on
+ *    distinct buffers are thread safe; overlapping calls on one cache race.
+ *  - fp16 data is passed as uint16_t bit patterns (IEEE binary16).
+ *  - Return value: MIKV_OK or an error code.  Argument validation happens on
+ *    the host before any launch; on a validation error nothing is launched
+ *    and nothing is written.  mikv_last_error() gives a message for the
+ *    calling thread's last error.  No call throws, aborts or prints.
+ *  - Overflow of a pool capacity can only be detected on the device (the
+ *    host does not know the pool fill levels); kernels then skip the
+ *    offending writes (never writing out of bounds) and OR a MIKV_DEVERR_*
+ *    bit into the cache's `status` word, which the caller may read.
+ *  - NaN or infinite inputs give unspecified (but in-bounds) results.
+ *  - head_dim must be 128.
+ */
+#ifndef MIKV_H
+#define MIKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum mikv_status {
+  MIKV_OK = 0,
+  MIKV_ERR_INVALID_ARG = 1, /* null pointer, bad shape or inconsistent sizes */
+  MIKV_ERR_UNSUPPORTED = 2, /* head_dim != 128, unsupported bit width / group / GQA group */
+  MIKV_ERR_CAPACITY = 3,    /* host-detectable capacity overflow (length > max_len, workspace too small) */
+  MIKV_ERR_HIP = 4          /* a HIP launch failed (hipGetLastError) */
+};
+
+/* Bits of mikv_cache.status, set on the device. */
+enum mikv_device_error {
+  MIKV_DEVERR_HI_FULL = 1, /* importance pool overflow: token not stored */
+  MIKV_DEVERR_LO_FULL = 2  /* retained pool overflow: token not stored */
+};
+
+/* Flags of mikv_decode_attention. */
+enum mikv_attention_flags {
+  /* Also add the step's probabilities of importance-pool tokens to their
+   * scores (the mikv_importance_update of the same step, fused). */
+  MIKV_ATTN_ACCUMULATE = 1
+};
+
+/*
+ * The cache of B sequences x Hkv KV heads.  NH = B * Hkv independent heads;
+ * head index h = b * Hkv + kv_head.  Every pool array is [NH, cap, ...]
+ * row-major.
+ *
+ * Importance pool (high precision, Section 3.3):
+ *   hi_bits == 16: hi_k, hi_v are fp16 [NH, cap_hi, 128]; hi_kp, hi_vp unused.
+ *   hi_bits == 8 : hi_k, hi_v are uint8 codes [NH, cap_hi, 128];
+ *                  hi_kp, hi_vp are fp16 (alpha, beta) pairs [NH, cap_hi, 128/group, 2].
+ *   hi_pos  [NH, cap_hi] int32: token position held by each slot.
+ *   hi_acc  [NH, cap_hi] fp32 : the token's accumulated attention (H2O score).
+ *   n_hi    [NH] int32        : occupied slots (slots [0, n_hi) are valid).
+ * Retained pool (low precision, Section 3.1):
+ *   lo_k, lo_v   uint8 packed codes [NH, cap_lo, 128 * lo_bits / 8];
+ *   lo_kp, lo_vp fp16 (alpha, beta) pairs [NH, cap_lo, 128/group, 2];
+ *   lo_pos [NH, cap_lo] int32; n_lo [NH] int32.
+ * Codes: Eq. 1 per token and per group of `group` contiguous channels, packed
+ * least-significant-bits first (channel c at byte c*N/8, bit (c*N)%8).
+ * Keys are stored balanced (Eq. 3) when a balancer is in use.
+ * map [NH, max_len] uint8 (nullable): 1 = position in the importance pool,
+ *   0 = retained pool; maintained by mikv_quantize_kv and mikv_select_topk.
+ * status: one device int32 (required), see mikv_device_error.
+ * Retained-pool tokens carry no score: they are never promoted again, so
+ * their score would never be read.
+ */
+typedef struct mikv_cache {
+  int32_t batch;
+  int32_t q_heads;
+  int32_t kv_heads;   /* q_heads % kv_heads == 0; q_heads / kv_heads in {1,2,4,8} */
+  int32_t head_dim;   /* 128 */
+  int32_t group;      /* quantization group size: 32, 64 or 128 channels */
+  int32_t hi_bits;    /* 16 (fp16) or 8 (INT8) */
+  int32_t lo_bits;    /* 2, 4 or 8 */
+  int32_t cap_hi;     /* importance-pool slots per head */
+  int32_t cap_lo;     /* retained-pool slots per head */
+  int32_t max_len;    /* positions per head (length of map rows) */
+  void *hi_k, *hi_v;
+  uint16_t *hi_kp, *hi_vp;
+  int32_t *hi_pos;
+  float *hi_acc;
+  int32_t *n_hi;
+  uint8_t *lo_k, *lo_v;
+  uint16_t *lo_kp, *lo_vp;
+  int32_t *lo_pos;
+  int32_t *n_lo;
+  uint8_t *map;
+  int32_t *status;
+} mikv_cache;
+
+/* Message describing the calling thread's last error ("" if none). */
+const char *mikv_last_error(void);
+
+/*
+ * Channel balancer, Section 3.2, Eq. 2:
+ *   balance[b, h, c] = sqrt( max_{t, i in group(h)} |q[b, i, t, c]| / max_t |k[b, h, t, c]| )
+ * over the prefill prompt, in fp32 (correctly rounded divide and square
+ * root); 1 where either maximum is 0.
+ *   q_prefill fp16 [B, Hq, T, 128]; k_prefill fp16 [B, Hkv, T, 128];
+ *   balance   fp32 [B, Hkv, 128] (output);
+ *   workspace device bytes, at least mikv_balance_workspace_size(B, Hkv, T).
+ * Errors: INVALID_ARG for null pointers, T < 1, Hq % Hkv != 0; UNSUPPORTED
+ * for head_dim != 128; CAPACITY for a too-small workspace.
+ */
+size_t mikv_balance_workspace_size(int32_t batch, int32_t kv_heads, int32_t tokens);
+int mikv_balance_channels(const uint16_t *q_prefill, const uint16_t *k_prefill, int32_t batch,
+                          int32_t q_heads, int32_t kv_heads, int32_t tokens, int32_t head_dim,
+                          float *balance, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Raw per-token grouped asymmetric quantizer, Section 3.1, Eq. 1, on rows of
+ * 128 channels (for unit use and testing):
+ *   x_c   = fp32(x[r, c]) * balance[r / rows_per_balance, c]   (balance nullable: x_c = fp32(x))
+ *   alpha = fp16((max x - min x) / (2^bits - 1)), beta = fp16(min x) per group,
+ *   code  = clamp(rint((x - beta) / alpha), 0, 2^bits - 1)  (all codes 0 if alpha == 0)
+ * with fp32 arithmetic, round half to even, a correctly rounded divide and
+ * the stored fp16 alpha and beta used for encoding.
+ *   x      fp16 [rows, 128];   balance fp32 [rows / rows_per_balance, 128] or NULL;
+ *   codes  uint8 [rows, 128 * bits / 8] (packed, LSB first);
+ *   params fp16 (alpha, beta) pairs [rows, 128 / group, 2].
+ * bits in {2, 4, 8}; group in {32, 64, 128}.  rows == 0 is a no-op (pointers may
+ * then be NULL).
+ */
+int mikv_quantize_rows(const uint16_t *x, int64_t rows, int32_t head_dim, const float *balance,
+                       int32_t rows_per_balance, int32_t bits, int32_t group, uint8_t *codes,
+                       uint16_t *params, void *stream);
+
+/*
+ * Place n consecutive tokens, positions pos0 .. pos0+n-1, of every head into
+ * the cache (prefill: the cache generated en masse, Section 2.1; decode: the
+ * new token's key/value added each generation step).
+ *   k, v       fp16 [B, Hkv, n, 128];
+ *   balance    fp32 [B, Hkv, 128] or NULL (Eq. 3: keys are multiplied by it
+ *              before quantization or fp16 storage; values are not balanced);
+ *   hi_mask    uint8 [B, Hkv, n] or NULL (NULL: every token to the importance
+ *              pool, as for a newly generated token);
+ *   score_init fp32 [B, Hkv, n] or NULL: initial score of tokens entering the
+ *              importance pool (NULL: 0, a new token's score).
+ * Tokens are appended to their pool after the occupied slots, in position
+ * order; hi_pos/lo_pos, n_hi/n_lo, hi_acc and map are updated.  Importance
+ * tokens are stored as fp16 (hi_bits 16: fp16 of the fp32 balanced key) or
+ * INT8 codes, retained tokens as lo_bits codes.
+ *   workspace: at least mikv_quantize_workspace_size(c, n) bytes (0 when
+ *   hi_mask is NULL).
+ * Errors: INVALID_ARG (null pointers, n < 1, pos0 < 0), CAPACITY (pos0 + n >
+ * max_len, workspace too small); pool overflow sets MIKV_DEVERR_* bits.
+ */
+size_t mikv_quantize_workspace_size(const mikv_cache *c, int32_t n);
+int mikv_quantize_kv(const mikv_cache *c, const uint16_t *k, const uint16_t *v, const float *balance,
+                     int32_t pos0, int32_t n, const uint8_t *hi_mask, const float *score_init,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Decode-step attention over the mixed-precision cache, Section 3.4 and
+ * Fig. 3 (left): K and V are dequantized on the fly (Eq. 1, alpha*code+beta,
+ * or the fp16 value), the query stays floating point (q / balance, Eq. 4):
+ *   s_j = (q_hat . k_j) * scale over every token j of both pools,
+ *   p   = softmax(s),   out = sum_j p_j v_j,
+ * accumulated in fp32, split over the sequence (split-K) and merged exactly.
+ *   length    tokens per head currently in the cache (host-known bound on
+ *             n_hi + n_lo; sizes the launch);
+ *   q         fp16 [B, Hq, 128];  balance fp32 [B, Hkv, 128] or NULL;
+ *   out       fp32 [B, Hq, 128];
+ *   probs_hi  fp32 [B, Hq, cap_hi] or NULL: probabilities of importance-pool
+ *             tokens, in slot order (entry [b, i, s] belongs to hi_pos[b*Hkv + i/G, s]);
+ *   probs_lo  fp32 [B, Hq, cap_lo] or NULL: the same for the retained pool;
+ *   flags     MIKV_ATTN_ACCUMULATE: also hi_acc[s] += sum over the group's
+ *             query heads of probs_hi (left to right in head order, then one
+ *             fp32 add) -- the importance update of this step, fused;
+ *   workspace at least mikv_decode_workspace_size(c, length) bytes.
+ * The call runs two phases that may also be launched separately:
+ * _partial (per-chunk scores, softmax partials and value sums) and
+ * _finalize (merge, probabilities, optional score update); both take the
+ * same arguments and must see the same ones.
+ * Errors: INVALID_ARG, UNSUPPORTED, CAPACITY (length > max_len, workspace).
+ */
+size_t mikv_decode_workspace_size(const mikv_cache *c, int32_t length);
+int mikv_decode_attention(const mikv_cache *c, int32_t length, const uint16_t *q,
+                          const float *balance, float scale, float *out, float *probs_hi,
+                          float *probs_lo, int32_t flags, void *workspace, size_t workspace_bytes,
+                          void *stream);
+int mikv_decode_attention_partial(const mikv_cache *c, int32_t length, const uint16_t *q,
+                                  const float *balance, float scale, float *out, float *probs_hi,
+                                  float *probs_lo, int32_t flags, void *workspace,
+                                  size_t workspace_bytes, void *stream);
+int mikv_decode_attention_finalize(const mikv_cache *c, int32_t length, const uint16_t *q,
+                                   const float *balance, float scale, float *out, float *probs_hi,
+                                   float *probs_lo, int32_t flags, void *workspace,
+                                   size_t workspace_bytes, void *stream);
+
+/*
+ * Importance update (the heavy-hitter accumulated attention policy MiKV
+ * adopts, Sections 3.1 and 4.1): for every occupied importance-pool slot s,
+ *   hi_acc[h, s] += ((probs_hi[b, hG, s] + probs_hi[b, hG+1, s]) + ...)
+ * summing the G query heads of the KV group left to right in fp32, then one
+ * fp32 add.  probs_hi as written by mikv_decode_attention.
+ * Errors: INVALID_ARG, CAPACITY (length > max_len).
+ */
+int mikv_importance_update(const mikv_cache *c, int32_t length, const float *probs_hi, void *stream);
+
+/*
+ * Re-rank and demote (Fig. 3 right, Section 3.1): per head, the recent
+ * window is positions [length - window, length); eligible tokens are the
+ * importance-pool tokens outside the window.  The k_heavy eligible tokens
+ * with the largest key (score, position) stay; every other eligible token is
+ * demoted: its stored high-precision key/value (fp16, or INT8 decoded in
+ * fp32) is re-quantized with Eq. 1 at lo_bits into the retained pool (keys
+ * are already balanced), its map entry set to 0, and its importance slot is
+ * refilled from the end of the pool.  Demotion is one way.
+ *   workspace at least mikv_select_workspace_size(c) bytes.
+ * Errors: INVALID_ARG (k_heavy < 0, window < 0, length > max_len), CAPACITY.
+ */
+size_t mikv_select_workspace_size(const mikv_cache *c);
+int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * First selection after prefill: every token outside the window is eligible.
+ *   scores  fp32 [n_heads, length] position-indexed initial scores;
+ *   hi_mask uint8 [n_heads, length] output: 1 for the window and for the
+ *           k_heavy eligible tokens with the largest key (score, position).
+ * Errors: INVALID_ARG.
+ */
+int mikv_select_prefill(const float *scores, int32_t n_heads, int32_t length, int32_t k_heavy,
+                        int32_t window, uint8_t *hi_mask, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MIKV_H */

@@ -1,0 +1,128 @@
+// Internal helpers of libmikv: device math shared by the kernels, and host
+// validation/error plumbing shared by the entry points.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <cstdarg>
+#include <cstdio>
+
+#include "../../include/mikv.h"
+
+namespace mikv {
+
+constexpr int kHeadDim = 128;
+
+// ---------------------------------------------------------------------------
+// Host: error reporting.
+// ---------------------------------------------------------------------------
+int set_error(int code, const char *fmt, ...);
+int check_launch(const char *what);
+
+// Validate a cache descriptor (host side, before any launch).
+int validate_cache(const mikv_cache *c);
+
+inline int group_size_of(const mikv_cache *c) { return c->q_heads / c->kv_heads; }
+inline int n_heads_of(const mikv_cache *c) { return c->batch * c->kv_heads; }
+
+// Bytes of one token (key + value, codes + fp16 params) in a pool of `bits`.
+inline int64_t token_bytes(int bits, int group) {
+  if (bits == 16) return 2 * kHeadDim * 2;
+  return 2 * (kHeadDim * bits / 8 + 4 * (kHeadDim / group));
+}
+
+// ---------------------------------------------------------------------------
+// Device: exact arithmetic helpers.
+// ---------------------------------------------------------------------------
+
+// fp32 -> fp16, round to nearest even, from the IEEE 754 binary16 definition
+// in integer arithmetic (exact also for fp16 subnormal results, independent
+// of the hardware conversion's denormal mode).
+__host__ __device__ inline uint16_t f32_to_f16_rne(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  uint32_t sign = (u >> 16) & 0x8000u;
+  uint32_t a = u & 0x7fffffffu;
+  if (a >= 0x7f800000u) return (uint16_t)(sign | 0x7c00u | (a > 0x7f800000u ? 0x200u : 0u));
+  if (a >= 0x477ff000u) return (uint16_t)(sign | 0x7c00u);  // rounds to infinity
+  if (a < 0x38800000u) {                                      // fp16 subnormal or zero
+    uint32_t e = a >> 23;
+    if (e < 102u) return (uint16_t)sign;                      // below half the smallest subnormal
+    uint32_t m = (a & 0x7fffffu) | 0x800000u;
+    uint32_t s = 126u - e;                                    // 14 .. 24
+    uint32_t r = m >> s;
+    uint32_t rem = m & ((1u << s) - 1u);
+    uint32_t half = 1u << (s - 1u);
+    if (rem > half || (rem == half && (r & 1u))) ++r;
+    return (uint16_t)(sign | r);
+  }
+  uint32_t r = ((a >> 23) - 112u) << 10 | ((a >> 13) & 0x3ffu);
+  uint32_t rem = a & 0x1fffu;
+  if (rem > 0x1000u || (rem == 0x1000u && (r & 1u))) ++r;
+  return (uint16_t)(sign | r);
+}
+
+__device__ inline float f16_to_f32(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+
+// Order-preserving map of an fp32 score to uint32 (-0 treated as +0).
+__device__ inline uint32_t ordered_bits(float f) {
+  uint32_t u = __builtin_bit_cast(uint32_t, f);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Eq. 1 parameters of one group from its min and max (fp32), exactly as the
+// stored format defines them.  The library is compiled with
+// -ffp-contract=off, so every operator below is one correctly rounded fp32
+// operation (division included: hipcc's default is the correctly rounded
+// fp32 divide and square root); fused multiply-adds are only those written
+// explicitly with fmaf.
+struct GroupParams {
+  uint16_t a16, b16;
+  float a, b;
+};
+
+__device__ inline GroupParams group_params(float mn, float mx, int bits) {
+  GroupParams p;
+  float top = (float)((1 << bits) - 1);
+  float alpha32 = (mx - mn) / top;
+  p.a16 = f32_to_f16_rne(alpha32);
+  p.b16 = f32_to_f16_rne(mn);
+  p.a = f16_to_f32(p.a16);
+  p.b = f16_to_f32(p.b16);
+  return p;
+}
+
+__device__ inline uint32_t encode(float x, const GroupParams &p, int bits) {
+  if (p.a == 0.0f) return 0u;
+  float t = rintf((x - p.b) / p.a);
+  float top = (float)((1 << bits) - 1);
+  t = fminf(fmaxf(t, 0.0f), top);
+  return (uint32_t)t;
+}
+
+// ---------------------------------------------------------------------------
+// Device: wave-level reductions (wave64).
+// ---------------------------------------------------------------------------
+template <int WIDTH>
+__device__ inline float sum_lanes(float v) {
+#pragma unroll
+  for (int o = WIDTH / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ inline float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace mikv

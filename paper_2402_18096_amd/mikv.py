@@ -1,0 +1,342 @@
+"""ctypes binding of libmikv.so (C ABI in include/mikv.h).
+
+Argument marshalling only: every function below forwards torch tensors'
+device pointers to the C entry point of the same name, on torch's current
+HIP stream, and raises :class:`MikvError` on a non-zero status.  All compute
+happens in the HIP kernels.  There is no fallback: if the library has not
+been built the first call raises.
+
+:class:`MikvCache` allocates the caller-owned buffers of one cache (torch
+tensors, so torch's allocator provides the device memory) and
+:class:`MikvDecoder` strings the calls into the prefill and decode-step
+sequence of the method.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from ctypes import c_float, c_int32, c_int64, c_size_t, c_void_p
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmikv.so")
+HEAD_DIM = 128
+ATTN_ACCUMULATE = 1
+DEVERR_HI_FULL = 1
+DEVERR_LO_FULL = 2
+
+
+class MikvError(RuntimeError):
+    pass
+
+
+class CacheDesc(ctypes.Structure):
+    """Mirror of ``struct mikv_cache``."""
+    _fields_ = [(n, c_int32) for n in ("batch", "q_heads", "kv_heads", "head_dim", "group", "hi_bits",
+                                       "lo_bits", "cap_hi", "cap_lo", "max_len")] + \
+               [(n, c_void_p) for n in ("hi_k", "hi_v", "hi_kp", "hi_vp", "hi_pos", "hi_acc", "n_hi",
+                                        "lo_k", "lo_v", "lo_kp", "lo_vp", "lo_pos", "n_lo", "map", "status")]
+
+
+_LIB = None
+_PC = ctypes.POINTER(CacheDesc)
+
+_SIGS = {
+    "mikv_last_error": (ctypes.c_char_p, []),
+    "mikv_balance_workspace_size": (c_size_t, [c_int32, c_int32, c_int32]),
+    "mikv_balance_channels": (c_int32, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_int32,
+                                        c_void_p, c_void_p, c_size_t, c_void_p]),
+    "mikv_quantize_rows": (c_int32, [c_void_p, c_int64, c_int32, c_void_p, c_int32, c_int32, c_int32,
+                                     c_void_p, c_void_p, c_void_p]),
+    "mikv_quantize_workspace_size": (c_size_t, [_PC, c_int32]),
+    "mikv_quantize_kv": (c_int32, [_PC, c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_void_p, c_void_p,
+                                   c_void_p, c_size_t, c_void_p]),
+    "mikv_decode_workspace_size": (c_size_t, [_PC, c_int32]),
+    "mikv_importance_update": (c_int32, [_PC, c_int32, c_void_p, c_void_p]),
+    "mikv_select_workspace_size": (c_size_t, [_PC]),
+    "mikv_select_topk": (c_int32, [_PC, c_int32, c_int32, c_int32, c_void_p, c_size_t, c_void_p]),
+    "mikv_select_prefill": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
+}
+for _n in ("mikv_decode_attention", "mikv_decode_attention_partial", "mikv_decode_attention_finalize"):
+    _SIGS[_n] = (c_int32, [_PC, c_int32, c_void_p, c_void_p, c_float, c_void_p, c_void_p, c_void_p, c_int32,
+                           c_void_p, c_size_t, c_void_p])
+
+EXPORTS = tuple(_SIGS)
+
+
+def lib():
+    """Load libmikv.so (after torch, so both share torch's HIP runtime)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise MikvError(f"{LIB_PATH} is missing: build it with `python -m paper_2402_18096_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _LIB = L
+    return _LIB
+
+
+def _check(rc: int, name: str):
+    if rc != 0:
+        raise MikvError(f"{name} failed with status {rc}: {lib().mikv_last_error().decode()}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise MikvError("tensors passed to libmikv must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _require(t: torch.Tensor, dtype, shape=None, name="tensor"):
+    if t.dtype != dtype:
+        raise MikvError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise MikvError(f"{name}: must be a device tensor")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise MikvError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)
+
+
+# -- cache ------------------------------------------------------------------------
+
+class MikvCache:
+    """Device buffers of one mixed-precision cache (see ``struct mikv_cache``)."""
+
+    def __init__(self, batch: int, q_heads: int, kv_heads: int, group: int, hi_bits: int, lo_bits: int,
+                 cap_hi: int, cap_lo: int, max_len: int, device="cuda", with_map: bool = True):
+        self.batch, self.q_heads, self.kv_heads = batch, q_heads, kv_heads
+        self.group, self.hi_bits, self.lo_bits = group, hi_bits, lo_bits
+        self.cap_hi, self.cap_lo, self.max_len = cap_hi, cap_lo, max_len
+        self.device = torch.device(device)
+        NH, D, ng = batch * kv_heads, HEAD_DIM, HEAD_DIM // group
+        z = lambda *s, dt: torch.zeros(*s, dtype=dt, device=self.device)
+        if hi_bits == 16:
+            self.hi_k, self.hi_v = z(NH, cap_hi, D, dt=torch.float16), z(NH, cap_hi, D, dt=torch.float16)
+            self.hi_kp = self.hi_vp = None
+        else:
+            self.hi_k, self.hi_v = z(NH, cap_hi, D, dt=torch.uint8), z(NH, cap_hi, D, dt=torch.uint8)
+            self.hi_kp, self.hi_vp = z(NH, cap_hi, ng, 2, dt=torch.int16), z(NH, cap_hi, ng, 2, dt=torch.int16)
+        self.hi_pos = z(NH, cap_hi, dt=torch.int32)
+        self.hi_acc = z(NH, cap_hi, dt=torch.float32)
+        self.n_hi = z(NH, dt=torch.int32)
+        row = D * lo_bits // 8
+        self.lo_k, self.lo_v = z(NH, cap_lo, row, dt=torch.uint8), z(NH, cap_lo, row, dt=torch.uint8)
+        self.lo_kp, self.lo_vp = z(NH, cap_lo, ng, 2, dt=torch.int16), z(NH, cap_lo, ng, 2, dt=torch.int16)
+        self.lo_pos = z(NH, cap_lo, dt=torch.int32)
+        self.n_lo = z(NH, dt=torch.int32)
+        self.map = z(NH, max_len, dt=torch.uint8) if with_map else None
+        self.status = z(1, dt=torch.int32)
+        p = lambda t: None if t is None else t.data_ptr()
+        self.desc = CacheDesc(batch, q_heads, kv_heads, D, group, hi_bits, lo_bits, cap_hi, cap_lo, max_len,
+                              p(self.hi_k), p(self.hi_v), p(self.hi_kp), p(self.hi_vp), p(self.hi_pos),
+                              p(self.hi_acc), p(self.n_hi), p(self.lo_k), p(self.lo_v), p(self.lo_kp),
+                              p(self.lo_vp), p(self.lo_pos), p(self.n_lo), p(self.map), p(self.status))
+
+    @property
+    def n_heads(self) -> int:
+        return self.batch * self.kv_heads
+
+    def ref(self):
+        return ctypes.byref(self.desc)
+
+    def packed_bytes(self, length: int, n_hi: int) -> int:
+        """Packed K/V bytes of the cache (codes + fp16 alpha/beta + fp16 values)
+        when every head holds `length` tokens, `n_hi` of them high precision."""
+        def tb(bits):
+            return 4 * HEAD_DIM if bits == 16 else 2 * (HEAD_DIM * bits // 8 + 4 * (HEAD_DIM // self.group))
+        return self.n_heads * (n_hi * tb(self.hi_bits) + (length - n_hi) * tb(self.lo_bits))
+
+
+# -- entry points -----------------------------------------------------------------
+
+def mikv_balance_channels(q_prefill: torch.Tensor, k_prefill: torch.Tensor, balance: torch.Tensor,
+                          workspace: Optional[torch.Tensor] = None):
+    B, Hq, T, D = q_prefill.shape
+    Hkv = k_prefill.shape[1]
+    _require(q_prefill, torch.float16, name="q_prefill")
+    _require(k_prefill, torch.float16, (B, Hkv, T, D), "k_prefill")
+    _require(balance, torch.float32, (B, Hkv, D), "balance")
+    L = lib()
+    nbytes = L.mikv_balance_workspace_size(B, Hkv, T)
+    ws = workspace if workspace is not None else _workspace(nbytes, q_prefill.device)
+    _check(L.mikv_balance_channels(_ptr(q_prefill), _ptr(k_prefill), B, Hq, Hkv, T, D, _ptr(balance), _ptr(ws),
+                                   ws.numel(), _stream()), "mikv_balance_channels")
+
+
+def mikv_quantize_rows(x: torch.Tensor, bits: int, group: int, codes: torch.Tensor, params: torch.Tensor,
+                       balance: Optional[torch.Tensor] = None, rows_per_balance: int = 1):
+    rows = x.numel() // HEAD_DIM
+    _require(x, torch.float16, name="x")
+    _require(codes, torch.uint8, name="codes")
+    if codes.numel() != rows * HEAD_DIM * bits // 8 or params.numel() != rows * (HEAD_DIM // group) * 2:
+        raise MikvError("mikv_quantize_rows: codes/params size mismatch")
+    _check(lib().mikv_quantize_rows(_ptr(x), rows, HEAD_DIM, _ptr(balance), rows_per_balance, bits, group,
+                                    _ptr(codes), _ptr(params), _stream()), "mikv_quantize_rows")
+
+
+def mikv_quantize_kv(cache: MikvCache, k: torch.Tensor, v: torch.Tensor, pos0: int,
+                     balance: Optional[torch.Tensor] = None, hi_mask: Optional[torch.Tensor] = None,
+                     score_init: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None):
+    n = k.shape[2]
+    shp = (cache.batch, cache.kv_heads, n, HEAD_DIM)
+    _require(k, torch.float16, shp, "k")
+    _require(v, torch.float16, shp, "v")
+    if hi_mask is not None:
+        _require(hi_mask, torch.uint8, shp[:3], "hi_mask")
+    if score_init is not None:
+        _require(score_init, torch.float32, shp[:3], "score_init")
+    L = lib()
+    ws = workspace
+    if ws is None and hi_mask is not None:
+        ws = _workspace(L.mikv_quantize_workspace_size(cache.ref(), n), k.device)
+    _check(L.mikv_quantize_kv(cache.ref(), _ptr(k), _ptr(v), _ptr(balance), pos0, n, _ptr(hi_mask),
+                              _ptr(score_init), _ptr(ws), 0 if ws is None else ws.numel(), _stream()),
+           "mikv_quantize_kv")
+
+
+def _attention(name, cache, length, q, out, probs_hi, probs_lo, balance, scale, flags, workspace):
+    _require(q, torch.float16, (cache.batch, cache.q_heads, HEAD_DIM), "q")
+    _require(out, torch.float32, (cache.batch, cache.q_heads, HEAD_DIM), "out")
+    if probs_hi is not None:
+        _require(probs_hi, torch.float32, (cache.batch, cache.q_heads, cache.cap_hi), "probs_hi")
+    if probs_lo is not None:
+        _require(probs_lo, torch.float32, (cache.batch, cache.q_heads, cache.cap_lo), "probs_lo")
+    L = lib()
+    ws = workspace if workspace is not None else _workspace(L.mikv_decode_workspace_size(cache.ref(), length),
+                                                            q.device)
+    scale = 1.0 / math.sqrt(HEAD_DIM) if scale is None else scale
+    _check(getattr(L, name)(cache.ref(), length, _ptr(q), _ptr(balance), scale, _ptr(out), _ptr(probs_hi),
+                            _ptr(probs_lo), flags, _ptr(ws), ws.numel(), _stream()), name)
+
+
+def mikv_decode_attention(cache, length, q, out, probs_hi=None, probs_lo=None, balance=None, scale=None,
+                          flags=0, workspace=None):
+    _attention("mikv_decode_attention", cache, length, q, out, probs_hi, probs_lo, balance, scale, flags, workspace)
+
+
+def mikv_decode_attention_partial(cache, length, q, out, probs_hi=None, probs_lo=None, balance=None, scale=None,
+                                  flags=0, workspace=None):
+    _attention("mikv_decode_attention_partial", cache, length, q, out, probs_hi, probs_lo, balance, scale, flags,
+               workspace)
+
+
+def mikv_decode_attention_finalize(cache, length, q, out, probs_hi=None, probs_lo=None, balance=None, scale=None,
+                                   flags=0, workspace=None):
+    _attention("mikv_decode_attention_finalize", cache, length, q, out, probs_hi, probs_lo, balance, scale, flags,
+               workspace)
+
+
+def mikv_decode_workspace_size(cache: MikvCache, length: int) -> int:
+    return int(lib().mikv_decode_workspace_size(cache.ref(), length))
+
+
+def mikv_importance_update(cache: MikvCache, length: int, probs_hi: torch.Tensor):
+    _require(probs_hi, torch.float32, (cache.batch, cache.q_heads, cache.cap_hi), "probs_hi")
+    _check(lib().mikv_importance_update(cache.ref(), length, _ptr(probs_hi), _stream()), "mikv_importance_update")
+
+
+def mikv_select_topk(cache: MikvCache, length: int, k_heavy: int, window: int,
+                     workspace: Optional[torch.Tensor] = None):
+    L = lib()
+    ws = workspace if workspace is not None else _workspace(L.mikv_select_workspace_size(cache.ref()),
+                                                            cache.device)
+    _check(L.mikv_select_topk(cache.ref(), length, k_heavy, window, _ptr(ws), ws.numel(), _stream()),
+           "mikv_select_topk")
+
+
+def mikv_select_prefill(scores: torch.Tensor, k_heavy: int, window: int, hi_mask: torch.Tensor):
+    H, T = scores.shape[0], scores.shape[-1]
+    _require(scores, torch.float32, name="scores")
+    _require(hi_mask, torch.uint8, tuple(scores.shape), "hi_mask")
+    _check(lib().mikv_select_prefill(_ptr(scores), scores.numel() // T, T, k_heavy, window, _ptr(hi_mask),
+                                     _stream()), "mikv_select_prefill")
+
+
+# -- the method's step sequence ---------------------------------------------------
+
+def heavy_budget(length: int, ratio_num: int, ratio_den: int, window: int, window_in_ratio: bool) -> int:
+    """High-precision tokens outside the window for a cache of `length`:
+    floor(ratio * length), less the window when it counts towards the ratio."""
+    k = (ratio_num * length) // ratio_den
+    if window_in_ratio:
+        k -= window
+    return max(0, k)
+
+
+class MikvDecoder:
+    """Prefill and decode steps of one workload on one GPU.
+
+    A decode step is: append the new token (mikv_quantize_kv), attention
+    (mikv_decode_attention, probabilities of both pools emitted), importance
+    update (mikv_importance_update, or fused into attention with
+    ``fused=True``) and re-rank/demote (mikv_select_topk).
+    """
+
+    def __init__(self, wl, max_len: Optional[int] = None, device="cuda", fused: bool = False,
+                 cap_slack: int = 64):
+        self.wl, self.device, self.fused = wl, torch.device(device), fused
+        self.max_len = max_len or (wl.context + wl.steps)
+        cap_hi = min(self.max_len, heavy_budget(self.max_len, wl.ratio_num, wl.ratio_den, wl.window,
+                                                wl.window_in_ratio) + wl.window + cap_slack)
+        self.cache = MikvCache(wl.batch, wl.q_heads, wl.kv_heads, wl.group, wl.hi_bits, wl.lo_bits, cap_hi,
+                               self.max_len, self.max_len, device)
+        c = self.cache
+        self.length = 0
+        self.balance = None
+        B, Hq = wl.batch, wl.q_heads
+        self.out = torch.zeros(B, Hq, HEAD_DIM, dtype=torch.float32, device=self.device)
+        self.probs_hi = torch.zeros(B, Hq, c.cap_hi, dtype=torch.float32, device=self.device)
+        self.probs_lo = torch.zeros(B, Hq, c.cap_lo, dtype=torch.float32, device=self.device)
+        L = lib()
+        ws = max(L.mikv_decode_workspace_size(c.ref(), n) for n in range(1, self.max_len + 1))
+        self.attn_ws = _workspace(ws, self.device)
+        self.sel_ws = _workspace(L.mikv_select_workspace_size(c.ref()), self.device)
+
+    def k_heavy(self, length: int) -> int:
+        wl = self.wl
+        return heavy_budget(length, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio)
+
+    def prefill(self, k: torch.Tensor, v: torch.Tensor, scores: torch.Tensor,
+                q_prefill: Optional[torch.Tensor] = None):
+        """k, v fp16 [B, Hkv, T, D]; scores fp32 [B, Hkv, T]; q_prefill fp16
+        [B, Hq, T, D] when the workload balances keys and queries."""
+        wl, T = self.wl, k.shape[2]
+        if wl.balanced:
+            self.balance = torch.empty(wl.batch, wl.kv_heads, HEAD_DIM, dtype=torch.float32, device=self.device)
+            mikv_balance_channels(q_prefill, k, self.balance)
+        mask = torch.empty(wl.batch, wl.kv_heads, T, dtype=torch.uint8, device=self.device)
+        mikv_select_prefill(scores, self.k_heavy(T), wl.window, mask)
+        mikv_quantize_kv(self.cache, k, v, 0, self.balance, mask, scores)
+        self.length = T
+
+    def step(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, emit_lo: bool = True,
+             after_attention=None):
+        """One decode step; q fp16 [B, Hq, D], k_new/v_new fp16 [B, Hkv, D].
+        ``after_attention`` (optional) is called between attention and the
+        importance update, e.g. to snapshot the slot-ordered probabilities."""
+        c = self.cache
+        mikv_quantize_kv(c, k_new.unsqueeze(2), v_new.unsqueeze(2), self.length, self.balance)
+        self.length += 1
+        L = self.length
+        flags = ATTN_ACCUMULATE if self.fused else 0
+        mikv_decode_attention(c, L, q, self.out, self.probs_hi, self.probs_lo if emit_lo else None,
+                              self.balance, None, flags, self.attn_ws)
+        if after_attention is not None:
+            after_attention()
+        if not self.fused:
+            mikv_importance_update(c, L, self.probs_hi)
+        mikv_select_topk(c, L, self.k_heavy(L), self.wl.window, self.sel_ws)
+        return self.out

@@ -1,0 +1,167 @@
+"""Helpers shared by the GPU parity tests: run the HIP path and the oracle on
+the same seeded inputs and compare.
+
+The GPU keeps each head's tokens in two pools in slot order, with a position
+array per pool; the oracle keeps them by position.  Slot order is not part
+of the method (attention is permutation invariant), so the comparison maps
+every GPU slot to its position and then compares, bit for bit, the set of
+high-precision positions, every stored code, fp16 value and fp16
+scale/zero, and the importance scores of the high-precision tokens (the only
+scores the method reads again).  Attention outputs and probabilities are
+compared within tolerance.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2402_18096_amd import mikv, workloads
+
+SCALE = 1.0 / math.sqrt(128.0)
+# Attention output tolerance (stated for the method's decode attention).
+O_ATOL, O_RTOL = 2e-3, 1e-3
+# Probabilities: fp32 scores and exponentials; derived bound, see the design notes.
+P_ATOL, P_RTOL = 1e-9, 1e-3
+
+
+def inputs(wl, steps, device="cpu"):
+    k, v = workloads.prefill_kv(wl, device)
+    sc = workloads.initial_scores(wl, device)
+    qp = workloads.prefill_queries(wl, device) if wl.balanced else None
+    q, kn, vn = workloads.decode_inputs(wl, steps, device)
+    return k, v, sc, qp, q, kn, vn
+
+
+def np16(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().contiguous().numpy().view(np.float16)
+
+
+def gather_gpu_state(c: mikv.MikvCache):
+    """Position-indexed copy of the GPU cache: dict of numpy arrays [NH, L...]."""
+    n_hi = c.n_hi.cpu().numpy()
+    n_lo = c.n_lo.cpu().numpy()
+    hi_pos = c.hi_pos.cpu().numpy()
+    lo_pos = c.lo_pos.cpu().numpy()
+    hk = c.hi_k.cpu().numpy().view(np.uint16 if c.hi_bits == 16 else np.uint8)
+    hv = c.hi_v.cpu().numpy().view(np.uint16 if c.hi_bits == 16 else np.uint8)
+    acc = c.hi_acc.cpu().numpy()
+    lk, lv = c.lo_k.cpu().numpy(), c.lo_v.cpu().numpy()
+    lkp = c.lo_kp.cpu().numpy().view(np.uint16)
+    lvp = c.lo_vp.cpu().numpy().view(np.uint16)
+    hkp = c.hi_kp.cpu().numpy().view(np.uint16) if c.hi_kp is not None else None
+    hvp = c.hi_vp.cpu().numpy().view(np.uint16) if c.hi_vp is not None else None
+    return dict(n_hi=n_hi, n_lo=n_lo, hi_pos=hi_pos, lo_pos=lo_pos, hk=hk, hv=hv, acc=acc, lk=lk, lv=lv, lkp=lkp,
+                lvp=lvp, hkp=hkp, hvp=hvp, map=None if c.map is None else c.map.cpu().numpy())
+
+
+def compare_state(c: mikv.MikvCache, orc: oracle.OracleCache, heads=None, tag=""):
+    """Bit-exact comparison of the GPU cache with the oracle's, by position."""
+    s = gather_gpu_state(c)
+    L = orc.length
+    gpu_heads = list(range(orc.n_heads)) if heads is None else list(heads)
+    for oh, gh in enumerate(gpu_heads):
+        nh, nl = int(s["n_hi"][gh]), int(s["n_lo"][gh])
+        hp = s["hi_pos"][gh, :nh]
+        lp = s["lo_pos"][gh, :nl]
+        assert nh + nl == L, f"{tag} head {gh}: {nh}+{nl} tokens, expected {L}"
+        pos_hi = np.zeros(L, bool)
+        pos_hi[hp] = True
+        assert len(set(hp.tolist()) | set(lp.tolist())) == L, f"{tag} head {gh}: positions not a partition"
+        np.testing.assert_array_equal(pos_hi, orc.is_hi[oh, :L], err_msg=f"{tag} head {gh}: precision map")
+        if s["map"] is not None:
+            np.testing.assert_array_equal(s["map"][gh, :L].astype(bool), pos_hi, err_msg=f"{tag} head {gh}: map")
+        # importance pool contents and scores
+        np.testing.assert_array_equal(s["hk"][gh, :nh], orc.hk[oh, hp], err_msg=f"{tag} head {gh}: hi K")
+        np.testing.assert_array_equal(s["hv"][gh, :nh], orc.hv[oh, hp], err_msg=f"{tag} head {gh}: hi V")
+        if orc.hi_bits == 8:
+            np.testing.assert_array_equal(s["hkp"][gh, :nh, :, 0], orc.hk_a[oh, hp], err_msg=f"{tag} hi K alpha")
+            np.testing.assert_array_equal(s["hkp"][gh, :nh, :, 1], orc.hk_b[oh, hp], err_msg=f"{tag} hi K beta")
+            np.testing.assert_array_equal(s["hvp"][gh, :nh, :, 0], orc.hv_a[oh, hp], err_msg=f"{tag} hi V alpha")
+            np.testing.assert_array_equal(s["hvp"][gh, :nh, :, 1], orc.hv_b[oh, hp], err_msg=f"{tag} hi V beta")
+        np.testing.assert_array_equal(s["acc"][gh, :nh].view(np.uint32), orc.acc[oh, hp].view(np.uint32),
+                                      err_msg=f"{tag} head {gh}: importance scores")
+        # retained pool: packed codes and fp16 scale/zero
+        bits = orc.lo_bits
+        np.testing.assert_array_equal(s["lk"][gh, :nl], oracle.pack(orc.lk[oh, lp], bits), err_msg=f"{tag} lo K codes")
+        np.testing.assert_array_equal(s["lv"][gh, :nl], oracle.pack(orc.lv[oh, lp], bits), err_msg=f"{tag} lo V codes")
+        np.testing.assert_array_equal(s["lkp"][gh, :nl, :, 0], orc.lk_a[oh, lp], err_msg=f"{tag} lo K alpha")
+        np.testing.assert_array_equal(s["lkp"][gh, :nl, :, 1], orc.lk_b[oh, lp], err_msg=f"{tag} lo K beta")
+        np.testing.assert_array_equal(s["lvp"][gh, :nl, :, 0], orc.lv_a[oh, lp], err_msg=f"{tag} lo V alpha")
+        np.testing.assert_array_equal(s["lvp"][gh, :nl, :, 1], orc.lv_b[oh, lp], err_msg=f"{tag} lo V beta")
+
+
+def probs_by_position(c: mikv.MikvCache, probs_hi, probs_lo, n_hi, n_lo, hi_pos, lo_pos, L):
+    """GPU probabilities (slot order) -> [NH, G, L] position order."""
+    G = c.q_heads // c.kv_heads
+    ph = probs_hi.cpu().numpy().reshape(c.n_heads, G, c.cap_hi)
+    pl = probs_lo.cpu().numpy().reshape(c.n_heads, G, c.cap_lo)
+    out = np.full((c.n_heads, G, L), np.nan, np.float32)
+    for h in range(c.n_heads):
+        out[h][:, hi_pos[h, :n_hi[h]]] = ph[h, :, :n_hi[h]]
+        out[h][:, lo_pos[h, :n_lo[h]]] = pl[h, :, :n_lo[h]]
+    return out
+
+
+class Lockstep:
+    """GPU decoder and oracle side by side on one workload."""
+
+    def __init__(self, wl, steps, fused=False, max_len=None):
+        self.wl, self.steps = wl, steps
+        self.k, self.v, self.sc, self.qp, self.q, self.kn, self.vn = inputs(wl, steps)
+        self.dec = mikv.MikvDecoder(wl, max_len=max_len or wl.context + steps, device="cuda", fused=fused)
+        NH, G = wl.n_heads, wl.group_size
+        self.orc = oracle.OracleCache(NH, G, self.dec.max_len, wl.hi_bits, wl.lo_bits, wl.group)
+        self.bal = None
+
+    def prefill(self):
+        wl, NH, T = self.wl, self.wl.n_heads, self.wl.context
+        self.dec.prefill(self.k.cuda(), self.v.cuda(), self.sc.cuda(),
+                         self.qp.cuda() if self.qp is not None else None)
+        if wl.balanced:
+            qp = np16(self.qp).reshape(wl.batch, wl.kv_heads, wl.group_size, T, 128).reshape(NH, wl.group_size, T, 128)
+            self.bal = oracle.balancer(qp, np16(self.k).reshape(NH, T, 128))
+            got = self.dec.balance.cpu().numpy().reshape(NH, 128)
+            np.testing.assert_array_equal(got.view(np.uint32), self.bal.view(np.uint32), err_msg="balancer")
+        kh = oracle.heavy_budget(T, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio)
+        self.orc.prefill(np16(self.k).reshape(NH, T, 128), np16(self.v).reshape(NH, T, 128),
+                         self.sc.numpy().reshape(NH, T), kh, wl.window, self.bal)
+        torch.cuda.synchronize()
+        compare_state(self.dec.cache, self.orc, tag="prefill")
+
+    def step(self, t, check_state=True):
+        wl, NH, G = self.wl, self.wl.n_heads, self.wl.group_size
+        snap = {}
+
+        def after_attention():
+            c = self.dec.cache
+            snap["n_hi"] = c.n_hi.cpu().numpy()
+            snap["n_lo"] = c.n_lo.cpu().numpy()
+            snap["hi_pos"] = c.hi_pos.cpu().numpy()
+            snap["lo_pos"] = c.lo_pos.cpu().numpy()
+            snap["p_hi"] = self.dec.probs_hi.clone()
+            snap["p_lo"] = self.dec.probs_lo.clone()
+            snap["out"] = self.dec.out.cpu().numpy()
+
+        self.dec.step(self.q[t].cuda(), self.kn[t].cuda(), self.vn[t].cuda(), after_attention=after_attention)
+        torch.cuda.synchronize()
+        L = self.dec.length
+        self.orc.append(np16(self.kn[t]).reshape(NH, 128), np16(self.vn[t]).reshape(NH, 128), self.bal)
+        o_ref, p_ref = self.orc.attend(np16(self.q[t]).reshape(NH, G, 128), SCALE, self.bal)
+        o_gpu = snap["out"].reshape(NH, G, 128)
+        np.testing.assert_allclose(o_gpu, o_ref, atol=O_ATOL, rtol=O_RTOL, err_msg=f"step {t}: attention output")
+        p_gpu = probs_by_position(self.dec.cache, snap["p_hi"], snap["p_lo"], snap["n_hi"], snap["n_lo"],
+                                  snap["hi_pos"], snap["lo_pos"], L)
+        assert not np.isnan(p_gpu).any(), f"step {t}: a position got no probability"
+        np.testing.assert_allclose(p_gpu, p_ref, atol=P_ATOL, rtol=P_RTOL, err_msg=f"step {t}: probabilities")
+        # importance update and selection fed with the GPU's probabilities
+        self.orc.accumulate(p_gpu)
+        kh = oracle.heavy_budget(L, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio)
+        self.orc.select(kh, wl.window)
+        if check_state:
+            compare_state(self.dec.cache, self.orc, tag=f"step {t}")
+        err_o = float(np.max(np.abs(o_gpu - o_ref)))
+        err_p = float(np.max(np.abs(p_gpu - p_ref) / np.maximum(np.abs(p_ref), 1e-30)))
+        return err_o, err_p

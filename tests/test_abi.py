@@ -1,0 +1,92 @@
+"""The C ABI on the CPU: libmikv.so loads, exports every symbol include/mikv.h
+declares, and rejects bad arguments on the host before launching anything
+(no GPU is needed for any of these calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+import torch  # noqa: F401  (loads the HIP runtime libmikv.so links against)
+
+from paper_2402_18096_amd import mikv
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "mikv.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(mikv.LIB_PATH), reason="libmikv.so not built")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(mikv_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    L = mikv.lib()
+    names = declared_symbols()
+    assert len(names) == 14
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(mikv.EXPORTS)
+
+
+def _desc(**kw):
+    d = dict(batch=1, q_heads=4, kv_heads=4, head_dim=128, group=32, hi_bits=16, lo_bits=2, cap_hi=8, cap_lo=8,
+             max_len=16)
+    d.update(kw)
+    c = mikv.CacheDesc()
+    for k, v in d.items():
+        setattr(c, k, v)
+    for f in ("hi_k", "hi_v", "hi_pos", "hi_acc", "n_hi", "lo_k", "lo_v", "lo_kp", "lo_vp", "lo_pos", "n_lo",
+              "status"):
+        setattr(c, f, 0x1000)  # never dereferenced: validation fails or nothing launches
+    return c
+
+
+def _call_attention(c, length=4, ws_bytes=1 << 30):
+    L = mikv.lib()
+    return L.mikv_decode_attention(ctypes.byref(c), length, ctypes.c_void_p(0x1000), None, 0.1,
+                                   ctypes.c_void_p(0x1000), None, None, 0, ctypes.c_void_p(0x1000), ws_bytes, None)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("head_dim", 64, 2), ("group", 48, 2), ("hi_bits", 4, 2), ("lo_bits", 3, 2),
+    ("q_heads", 6, 1), ("kv_heads", 0, 1), ("cap_hi", 0, 1), ("batch", 0, 1),
+])
+def test_cache_validation_errors(field, value, code):
+    c = _desc(**{field: value})
+    assert _call_attention(c) == code
+    assert mikv.lib().mikv_last_error()
+
+
+def test_gqa_group_must_be_power_of_two_up_to_8():
+    assert _call_attention(_desc(q_heads=12, kv_heads=4)) == 2   # G = 3
+    assert _call_attention(_desc(q_heads=64, kv_heads=4)) == 2   # G = 16
+
+
+def test_null_pointers_and_capacity():
+    L = mikv.lib()
+    c = _desc()
+    c.n_hi = 0
+    assert _call_attention(c) == 1
+    c = _desc()
+    assert _call_attention(c, length=17) == 3        # length > max_len
+    assert _call_attention(c, ws_bytes=16) == 3      # workspace too small
+    assert L.mikv_quantize_rows(None, 4, 128, None, 1, 2, 32, None, None, None) == 1
+    assert L.mikv_quantize_rows(ctypes.c_void_p(1), 4, 128, None, 1, 3, 32, ctypes.c_void_p(1),
+                                ctypes.c_void_p(1), None) == 2
+    assert L.mikv_select_topk(ctypes.byref(_desc()), 4, -1, 0, ctypes.c_void_p(1), 1 << 20, None) == 1
+    assert L.mikv_select_prefill(None, 1, 4, 1, 1, None, None) == 1
+    assert L.mikv_balance_channels(ctypes.c_void_p(1), ctypes.c_void_p(1), 1, 4, 4, 8, 64, ctypes.c_void_p(1),
+                                   ctypes.c_void_p(1), 1 << 20, None) == 2
+    assert L.mikv_importance_update(ctypes.byref(_desc()), 4, None, None) == 1
+    qk = ctypes.c_void_p(0x1000)
+    assert L.mikv_quantize_kv(ctypes.byref(_desc()), qk, qk, None, 10, 8, None, None, None, 0, None) == 3
+
+
+def test_workspace_sizes_are_consistent():
+    L = mikv.lib()
+    c = _desc(cap_hi=100, cap_lo=1000, max_len=1000)
+    a = L.mikv_decode_workspace_size(ctypes.byref(c), 500)
+    assert a >= 4 * 4 * 100   # at least the scores scratch of the importance pool
+    assert L.mikv_select_workspace_size(ctypes.byref(c)) == 2 * 4 * 1 * 4 * 100
+    assert L.mikv_balance_workspace_size(1, 4, 1000) > 0

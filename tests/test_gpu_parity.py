@@ -1,0 +1,184 @@
+"""Parity of the HIP path with the oracle on the GPU.
+
+Every call goes through the C ABI (the ctypes binding).  Bit-exact: codes,
+fp16 scale/zero, fp16 values, balancer, precision maps, importance scores.
+Tolerance: attention output (2e-3 abs / 1e-3 rel) and probabilities.
+Workloads are the five configurations at reduced sizes (several chunks per
+pool with ragged tails), plus edge cases.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2402_18096_amd import mikv, workloads
+from tests.parity import Lockstep, compare_state, np16
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return torch.device("cuda:0")
+
+
+# -- raw quantizer ----------------------------------------------------------------
+
+def _adversarial_rows(rng, rows):
+    x = rng.standard_normal((rows, 128)).astype(np.float32) * 2
+    x[0::7] += 1000.3                          # offset-dominated groups (clamp)
+    x[1::7] *= 1e-6                            # fp16-subnormal alpha and beta
+    x[2::7] = np.round(x[2::7] * 2) / 2        # many exact ties
+    x[3::7, :64] = 0.7                         # degenerate groups
+    x[4::7] *= 500                             # large magnitudes
+    x[5::7] = rng.integers(0, 256, (len(x[5::7]), 128))  # integer-valued
+    return x.astype(np.float16)
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("group", [32, 64, 128])
+@pytest.mark.parametrize("balanced", [False, True])
+def test_quantize_rows_bit_exact(bits, group, balanced):
+    dev = _dev()
+    rng = np.random.default_rng(bits * 1000 + group + balanced)
+    rows = 4099
+    x = _adversarial_rows(rng, rows)
+    bal = None
+    rpb = 64
+    if balanced:
+        bal = (2.0 ** rng.uniform(-3, 3, ((rows + rpb - 1) // rpb, 128))).astype(np.float32)
+    codes = torch.empty(rows, 128 * bits // 8, dtype=torch.uint8, device=dev)
+    params = torch.empty(rows, 128 // group, 2, dtype=torch.int16, device=dev)
+    mikv.mikv_quantize_rows(torch.from_numpy(x.view(np.int16)).to(dev).view(torch.float16), bits, group, codes,
+                            params, None if bal is None else torch.from_numpy(bal).to(dev), rpb)
+    torch.cuda.synchronize()
+    xf = x.astype(np.float32)
+    if bal is not None:
+        xf = xf * np.repeat(bal, rpb, axis=0)[:rows]
+    c_ref, a_ref, b_ref = oracle.quantize(xf, bits, group)
+    np.testing.assert_array_equal(codes.cpu().numpy(), oracle.pack(c_ref, bits))
+    p = params.cpu().numpy().view(np.uint16)
+    np.testing.assert_array_equal(p[..., 0], a_ref)
+    np.testing.assert_array_equal(p[..., 1], b_ref)
+
+
+def test_quantize_rows_empty_is_noop():
+    dev = _dev()
+    codes = torch.zeros(1, 32, dtype=torch.uint8, device=dev)
+    params = torch.zeros(1, 4, 2, dtype=torch.int16, device=dev)
+    x = torch.zeros(0, 128, dtype=torch.float16, device=dev)
+    mikv.lib()
+    rc = mikv.lib().mikv_quantize_rows(mikv._ptr(x), 0, 128, None, 1, 2, 32, mikv._ptr(codes), mikv._ptr(params),
+                                       mikv._stream())
+    assert rc == 0
+
+
+# -- balancer -------------------------------------------------------------------------
+
+@pytest.mark.parametrize("G", [1, 4])
+def test_balancer_bit_exact(G):
+    dev = _dev()
+    rng = np.random.default_rng(G)
+    B, Hkv, T = 2, 3, 1500
+    q = (rng.standard_normal((B, Hkv * G, T, 128)) * np.where(np.arange(128) % 17 == 0, 25, 1)).astype(np.float16)
+    k = rng.standard_t(4, (B, Hkv, T, 128)).astype(np.float16)
+    q[0, :G, :, 5] = 0      # zero query channel -> b = 1
+    k[1, 2, :, 9] = 0       # zero key channel -> b = 1
+    out = torch.empty(B, Hkv, 128, dtype=torch.float32, device=dev)
+    tq = torch.from_numpy(q.view(np.int16)).to(dev).view(torch.float16)
+    tk = torch.from_numpy(k.view(np.int16)).to(dev).view(torch.float16)
+    mikv.mikv_balance_channels(tq, tk, out)
+    torch.cuda.synchronize()
+    ref = oracle.balancer(q.reshape(B, Hkv, G, T, 128), k)
+    np.testing.assert_array_equal(out.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
+# -- selection -------------------------------------------------------------------------
+
+@pytest.mark.parametrize("L,k,W", [(1000, 150, 32), (5000, 900, 128), (300, 0, 10), (300, 500, 10), (64, 10, 100),
+                                   (33000, 3000, 128)])
+def test_select_prefill_matches_oracle(L, k, W):
+    dev = _dev()
+    rng = np.random.default_rng(L + k)
+    H = 5
+    sc = (rng.integers(0, 50, (H, L)) / 64).astype(np.float32)   # many exact ties
+    sc[0] = rng.random(L).astype(np.float32)
+    sc[1, ::3] = -0.0
+    mask = torch.empty(H, L, dtype=torch.uint8, device=dev)
+    mikv.mikv_select_prefill(torch.from_numpy(sc).to(dev), k, W, mask)
+    torch.cuda.synchronize()
+    got = mask.cpu().numpy().astype(bool)
+    for h in range(H):
+        np.testing.assert_array_equal(got[h], oracle.select(sc[h], None, L, k, W, initial=True))
+
+
+# -- lock-step decode ------------------------------------------------------------------
+
+SMALL = {
+    "tiny": dict(),
+    "llama2_7b": dict(batch=2, q_heads=3, kv_heads=3, context=1500),
+    "llama2_13b": dict(batch=2, q_heads=3, kv_heads=3, context=1700),
+    "mistral_7b": dict(batch=2, q_heads=8, kv_heads=2, context=2300),
+    "long_context": dict(batch=1, q_heads=3, kv_heads=3, context=4100),
+}
+
+
+@pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
+@pytest.mark.parametrize("fused", [False, True])
+def test_lockstep_decode(name, fused):
+    _dev()
+    wl = workloads.small_workload(name, **SMALL[name])
+    steps = 6
+    run = Lockstep(wl, steps, fused=fused)
+    run.prefill()
+    for t in range(steps):
+        run.step(t)
+
+
+def test_lockstep_gqa8():
+    """Eight query heads per KV head (Llama-2-70b's grouping)."""
+    _dev()
+    wl = workloads.small_workload("mistral_7b", batch=1, q_heads=16, kv_heads=2, context=900)
+    run = Lockstep(wl, 4)
+    run.prefill()
+    for t in range(4):
+        run.step(t)
+
+
+def test_lockstep_window_outside_ratio_many_demotions():
+    """Budget shrinking faster than one token per step (window counted on top
+    of a ratio that the workload then lowers) exercises the radix-select path
+    of the re-rank with several demotions per head."""
+    _dev()
+    wl = workloads.small_workload("long_context", batch=1, q_heads=2, kv_heads=2, context=2000, ratio_num=1,
+                                  ratio_den=4)
+    run = Lockstep(wl, 3)
+    run.prefill()
+    run.step(0)
+    run.wl = wl.with_(ratio_den=6)            # budget drops from ~25 % to ~17 %
+    run.dec.wl = run.wl
+    run.step(1)
+    run.step(2)
+
+
+@pytest.mark.parametrize("ratio", [(0, 1), (1, 1)])
+def test_lockstep_single_pool(ratio):
+    """Ratio 0 and window 0 (every token retained at low precision: uniform
+    RTN) and ratio 1 (every token at high precision)."""
+    _dev()
+    wl = workloads.small_workload("tiny", context=700, ratio_num=ratio[0], ratio_den=ratio[1],
+                                  window=0 if ratio[0] == 0 else 32)
+    run = Lockstep(wl, 3)
+    run.prefill()
+    for t in range(3):
+        run.step(t)
+
+
+def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
+    dev = _dev()
+    c = mikv.MikvCache(1, 2, 2, 32, 16, 2, cap_hi=4, cap_lo=8, max_len=64, device=dev)
+    k = torch.randn(1, 2, 6, 128, device=dev).half()
+    mikv.mikv_quantize_kv(c, k, k.clone(), 0)    # six tokens into a 4-slot importance pool
+    torch.cuda.synchronize()
+    assert int(c.status.item()) & mikv.DEVERR_HI_FULL
+    assert c.n_hi.cpu().tolist() == [4, 4]
