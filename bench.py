@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Decode-step throughput of the MiKV mixed-precision KV cache on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the whole decode hot path over the batch: append the
+new token (quantize), attention over both precision pools with probability
+emission, importance update (fused into attention by default; --fused 0
+runs it as its own kernel), top-k re-rank with demotion/requantization.
+Inputs are synthetic, seeded, drawn directly in device memory, and resident
+before the timed region starts.  Prints ONE JSON line on stdout:
+
+  value      effective GB/s = packed K/V bytes the steps read (codes + fp16
+             scale/zero + fp16 values, both pools) / wall time of the K steps;
+  roofline   the attention partial kernel (the dominant one): its algorithmic
+             bytes per launch (the packed K/V bytes) / its mean duration from
+             HIP events recorded on its stream, against 8 TB/s;
+  cpu_baseline  the CPU oracle timed on a bounded sample of the same workload.
+
+Only one GPU is used; --gpus above 1 exits with an error.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def track_counts(dec, n_hi, length):
+    """Importance-pool size after one more step (append, then re-rank): the
+    window is always high precision, eligible tokens beyond k_heavy demote."""
+    L = length + 1
+    n_attn = n_hi + 1
+    elig = n_attn - min(dec.wl.window, L)
+    n_new = n_attn - max(0, elig - dec.k_heavy(L))
+    return L, n_attn, n_new
+
+
+def cpu_baseline(wl, steps_inputs, budget_s: float):
+    """The oracle, as it is, on a bounded sample: two (sequence, KV head)
+    pairs of batch element 0, decode steps until the time budget is used."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2402_18096_amd import workloads
+    from threadpoolctl import threadpool_info
+
+    q, kn, vn = steps_inputs
+    heads = sorted({0, wl.kv_heads // 2})
+    G, T = wl.group_size, wl.context
+    k, v = workloads.prefill_kv(wl, q.device, batches=range(1))
+    sc = workloads.initial_scores(wl, "cpu")[0].numpy()
+    f16 = lambda t: t.detach().cpu().contiguous().numpy().view(np.float16)
+    kk, vv = f16(k[0])[heads], f16(v[0])[heads]
+    bal = None
+    if wl.balanced:
+        qp = f16(workloads.prefill_queries(wl, q.device, batches=range(1))[0])
+        qp = qp.reshape(wl.kv_heads, G, T, 128)[heads]
+        bal = oracle.balancer(qp, kk)
+    n_steps = q.shape[0]
+    orc = oracle.OracleCache(len(heads), G, T + n_steps, wl.hi_bits, wl.lo_bits, wl.group)
+    orc.prefill(kk, vv, sc[heads], oracle.heavy_budget(T, wl.ratio_num, wl.ratio_den, wl.window,
+                                                       wl.window_in_ratio), wl.window, bal)
+    qh = [h * G + i for h in heads for i in range(G)]
+    tb = lambda bits: 4 * 128 if bits == 16 else 2 * (128 * bits // 8 + 4 * (128 // wl.group))
+    done, nbytes, t0 = 0, 0, time.perf_counter()
+    while done < n_steps and time.perf_counter() - t0 < budget_s:
+        L = orc.length + 1
+        n_hi = int(orc.is_hi[:, :L - 1].sum()) + len(heads)
+        nbytes += n_hi * tb(wl.hi_bits) + (len(heads) * L - n_hi) * tb(wl.lo_bits)
+        orc.step(f16(q[done, 0])[qh].reshape(len(heads), G, 128), f16(kn[done, 0])[heads], f16(vn[done, 0])[heads],
+                 1.0 / math.sqrt(128.0),
+                 oracle.heavy_budget(L, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio), wl.window, bal)
+        done += 1
+    el = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{len(heads)} of {wl.n_heads} (sequence, KV head) pairs x {done} decode steps "
+                      f"({el:.1f} s); numpy oracle, BLAS threads = {threads}",
+            "s_per_step_per_head": round(el / max(done, 1) / len(heads), 4)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="long_context")
+    ap.add_argument("--fused", type=int, default=1, help="fuse the importance update into attention (default 1)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="time budget of the CPU oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on exactly one GPU (asked for --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "this build measures one GPU's share and has no multi-GPU path.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2402_18096_amd import mikv, workloads
+
+    wl = workloads.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    n_total = args.warmup + args.steps
+    t_setup = time.perf_counter()
+    dec = mikv.MikvDecoder(wl, max_len=wl.context + n_total, device=dev, fused=bool(args.fused))
+    k, v = workloads.prefill_kv(wl, dev)
+    sc = workloads.initial_scores(wl, dev)
+    qp = workloads.prefill_queries(wl, dev) if wl.balanced else None
+    steps_inputs = workloads.decode_inputs(wl, n_total, dev)
+    q, kn, vn = steps_inputs
+    dec.prefill(k, v, sc, qp)
+    del k, v, qp
+    torch.cuda.synchronize()
+    log(f"[bench] {wl.name}: prefill of {wl.context} tokens x {wl.n_heads} heads done "
+        f"({time.perf_counter() - t_setup:.1f} s); warmup {args.warmup}, timed {args.steps}")
+
+    for t in range(args.warmup):
+        dec.step_native(q[t], kn[t], vn[t])
+    torch.cuda.synchronize()
+
+    n_hi = int(dec.cache.n_hi[0].item())
+    length = dec.length
+    step_bytes = []
+    for _ in range(args.steps):
+        length, n_attn, n_hi = track_counts(dec, n_hi, length)
+        step_bytes.append(dec.cache.packed_bytes(length, n_attn))
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    for evs in events:
+        for e in evs:
+            e.record()
+    torch.cuda.synchronize()
+
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        t = args.warmup + i
+        dec.step_native(q[t], kn[t], vn[t], phase_events=events[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    nh_dev = dec.cache.n_hi.cpu()
+    status = int(dec.cache.status.item())
+    if status != 0 or not bool((nh_dev == n_hi).all()):
+        log(f"[bench] ERROR: device status {status}, n_hi {nh_dev[:4].tolist()} vs tracked {n_hi}")
+        sys.exit(1)
+
+    phases = ["append", "attn_partial", "attn_finalize", "importance", "select"]
+    dur = {p: [events[i][j].elapsed_time(events[i][j + 1]) for i in range(args.steps)] for j, p in enumerate(phases)}
+    mean = lambda xs: sum(xs) / len(xs)
+    total_bytes = sum(step_bytes)
+    value = total_bytes / elapsed / 1e9
+    ms = elapsed / args.steps * 1e3
+    part_ms = mean(dur["attn_partial"])
+    attn_ms = mean([a + b for a, b in zip(dur["attn_partial"], dur["attn_finalize"])])
+    mean_bytes = total_bytes / args.steps
+    achieved = mean_bytes / (part_ms * 1e-3) / 1e9
+    log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms: {ms * 1e3:.1f} us/step, "
+        f"{value:.1f} GB/s effective ({100 * value / HBM_PEAK_GBPS:.1f} % of peak)")
+    log("[bench] phase means (us): " + ", ".join(f"{p} {mean(dur[p]) * 1e3:.1f}" for p in phases))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, steps_inputs, args.cpu_seconds)
+        log(f"[bench] cpu oracle: {cpu['value']} GB/s ({cpu['sample']})")
+
+    rec = {
+        "metric": "mixed-KV decode attention effective GB/s (% of HBM peak) + decode steps/s",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "q_heads": wl.q_heads, "kv_heads": wl.kv_heads,
+                   "head_dim": wl.head_dim, "context": wl.context, "hi_bits": wl.hi_bits, "lo_bits": wl.lo_bits,
+                   "group": wl.group, "ratio": f"{wl.ratio_num}/{wl.ratio_den}", "window": wl.window,
+                   "balanced": wl.balanced, "importance_fused": bool(args.fused),
+                   "parallelism": "single GPU"},
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "steps_per_s": round(1e3 / ms, 1),
+        "attention_GBps": round(mean_bytes / (attn_ms * 1e-3) / 1e9, 2),
+        "packed_bytes_per_step": int(mean_bytes),
+        "phase_us": {p: round(mean(dur[p]) * 1e3, 2) for p in phases},
+        "roofline": {"kernel": "attn_partial_kernel", "bound": "hbm", "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -247,6 +247,28 @@ int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32
 int mikv_select_prefill(const float *scores, int32_t n_heads, int32_t length, int32_t k_heavy,
                         int32_t window, uint8_t *hi_mask, void *stream);
 
+/*
+ * One whole decode step (Fig. 3, generation phase) in a single call, in the
+ * order attend, accumulate, then demote:
+ *   1. mikv_quantize_kv of the new token (position length - 1, importance pool);
+ *   2. mikv_decode_attention over `length` tokens;
+ *   3. mikv_importance_update (skipped when MIKV_ATTN_ACCUMULATE fuses it into 2);
+ *   4. mikv_select_topk(k_heavy, window).
+ *   q fp16 [B, Hq, 128]; k_new, v_new fp16 [B, Hkv, 128]; other arguments as
+ *   in the calls above (probs_hi is required unless MIKV_ATTN_ACCUMULATE).
+ *   workspace    at least mikv_decode_step_workspace_size(c, length) bytes;
+ *   phase_events NULL, or 6 hipEvent_t (entries may be NULL) recorded on
+ *                `stream` before step 1 and after steps 1, 2 (partial
+ *                phase), 2 (finalize phase), 3 and 4, for profiling.
+ * Errors: those of the four calls, checked before the first launch where the
+ * host can check them.
+ */
+size_t mikv_decode_step_workspace_size(const mikv_cache *c, int32_t length);
+int mikv_decode_step(const mikv_cache *c, int32_t length, const uint16_t *q, const uint16_t *k_new,
+                     const uint16_t *v_new, const float *balance, float scale, float *out, float *probs_hi,
+                     float *probs_lo, int32_t k_heavy, int32_t window, int32_t flags, void *workspace,
+                     size_t workspace_bytes, void *const *phase_events, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,0 +1,62 @@
+// One whole decode step of the method in one call (Fig. 3): append the new
+// token, attention over both pools, importance update, re-rank and demote.
+// A single host call keeps the step from being bound by per-call host
+// overhead; optional events mark the phase boundaries for profiling.
+#include <algorithm>
+
+#include "mikv_internal.h"
+
+using namespace mikv;
+
+extern "C" size_t mikv_decode_step_workspace_size(const mikv_cache *c, int32_t length) {
+  size_t a = mikv_decode_workspace_size(c, length);
+  if (!a) return 0;
+  size_t s = mikv_select_workspace_size(c);
+  return ((a + 255) / 256) * 256 + s;
+}
+
+extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint16_t *q, const uint16_t *k_new,
+                                const uint16_t *v_new, const float *balance, float scale, float *out, float *probs_hi,
+                                float *probs_lo, int32_t k_heavy, int32_t window, int32_t flags, void *workspace,
+                                size_t workspace_bytes, void *const *phase_events, void *stream) {
+  int rc = validate_cache(c);
+  if (rc) return rc;
+  if (!q || !k_new || !v_new || !out) return set_error(MIKV_ERR_INVALID_ARG, "mikv_decode_step: NULL input/output");
+  if (length < 1 || length > c->max_len)
+    return set_error(length < 1 ? MIKV_ERR_INVALID_ARG : MIKV_ERR_CAPACITY,
+                     "mikv_decode_step: length %d outside [1, max_len]", length);
+  if (k_heavy < 0 || window < 0) return set_error(MIKV_ERR_INVALID_ARG, "mikv_decode_step: negative k_heavy/window");
+  const bool fused = (flags & MIKV_ATTN_ACCUMULATE) != 0;
+  if (!fused && !probs_hi)
+    return set_error(MIKV_ERR_INVALID_ARG, "mikv_decode_step: probs_hi is required unless MIKV_ATTN_ACCUMULATE");
+  const size_t need = mikv_decode_step_workspace_size(c, length);
+  if (!workspace || workspace_bytes < need)
+    return set_error(MIKV_ERR_CAPACITY, "mikv_decode_step: workspace too small (%zu < %zu)", workspace_bytes, need);
+  const size_t attn_ws = ((mikv_decode_workspace_size(c, length) + 255) / 256) * 256;
+  uint8_t *ws = (uint8_t *)workspace;
+  hipStream_t st = (hipStream_t)stream;
+  auto mark = [&](int i) {
+    if (phase_events && phase_events[i]) hipEventRecord((hipEvent_t)phase_events[i], st);
+  };
+  mark(0);
+  rc = mikv_quantize_kv(c, k_new, v_new, balance, length - 1, 1, nullptr, nullptr, nullptr, 0, stream);
+  if (rc) return rc;
+  mark(1);
+  rc = mikv_decode_attention_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws,
+                                     stream);
+  if (rc) return rc;
+  mark(2);
+  rc = mikv_decode_attention_finalize(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws,
+                                      stream);
+  if (rc) return rc;
+  mark(3);
+  if (!fused) {
+    rc = mikv_importance_update(c, length, probs_hi, stream);
+    if (rc) return rc;
+  }
+  mark(4);
+  rc = mikv_select_topk(c, length, k_heavy, window, ws + attn_ws, workspace_bytes - attn_ws, stream);
+  if (rc) return rc;
+  mark(5);
+  return MIKV_OK;
+}

@@ -63,6 +63,11 @@ for _n in ("mikv_decode_attention", "mikv_decode_attention_partial", "mikv_decod
     _SIGS[_n] = (c_int32, [_PC, c_int32, c_void_p, c_void_p, c_float, c_void_p, c_void_p, c_void_p, c_int32,
                            c_void_p, c_size_t, c_void_p])
 
+_SIGS["mikv_decode_step_workspace_size"] = (c_size_t, [_PC, c_int32])
+_SIGS["mikv_decode_step"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_float, c_void_p,
+                                       c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p, c_size_t, c_void_p,
+                                       c_void_p])
+
 EXPORTS = tuple(_SIGS)
 
 
@@ -265,6 +270,27 @@ def mikv_select_prefill(scores: torch.Tensor, k_heavy: int, window: int, hi_mask
                                      _stream()), "mikv_select_prefill")
 
 
+def mikv_decode_step(cache: MikvCache, length: int, q, k_new, v_new, out, k_heavy: int, window: int,
+                     probs_hi=None, probs_lo=None, balance=None, scale=None, flags=0, workspace=None,
+                     phase_events=None):
+    """Whole decode step in one native call; ``phase_events`` is an optional
+    sequence of 6 ``torch.cuda.Event`` (already recorded once, so they exist)."""
+    _require(q, torch.float16, (cache.batch, cache.q_heads, HEAD_DIM), "q")
+    _require(k_new, torch.float16, (cache.batch, cache.kv_heads, HEAD_DIM), "k_new")
+    _require(v_new, torch.float16, (cache.batch, cache.kv_heads, HEAD_DIM), "v_new")
+    _require(out, torch.float32, (cache.batch, cache.q_heads, HEAD_DIM), "out")
+    L = lib()
+    ws = workspace if workspace is not None else _workspace(L.mikv_decode_step_workspace_size(cache.ref(), length),
+                                                            q.device)
+    ev = None
+    if phase_events is not None:
+        ev = (c_void_p * 6)(*[e.cuda_event if e is not None else None for e in phase_events])
+    scale = 1.0 / math.sqrt(HEAD_DIM) if scale is None else scale
+    _check(L.mikv_decode_step(cache.ref(), length, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(balance), scale,
+                              _ptr(out), _ptr(probs_hi), _ptr(probs_lo), k_heavy, window, flags, _ptr(ws),
+                              ws.numel(), ev, _stream()), "mikv_decode_step")
+
+
 # -- the method's step sequence ---------------------------------------------------
 
 def heavy_budget(length: int, ratio_num: int, ratio_den: int, window: int, window_in_ratio: bool) -> int:
@@ -304,6 +330,8 @@ class MikvDecoder:
         ws = max(L.mikv_decode_workspace_size(c.ref(), n) for n in range(1, self.max_len + 1))
         self.attn_ws = _workspace(ws, self.device)
         self.sel_ws = _workspace(L.mikv_select_workspace_size(c.ref()), self.device)
+        sws = max(L.mikv_decode_step_workspace_size(c.ref(), n) for n in range(1, self.max_len + 1))
+        self.step_ws = _workspace(sws, self.device)
 
     def k_heavy(self, length: int) -> int:
         wl = self.wl
@@ -339,4 +367,14 @@ class MikvDecoder:
         if not self.fused:
             mikv_importance_update(c, L, self.probs_hi)
         mikv_select_topk(c, L, self.k_heavy(L), self.wl.window, self.sel_ws)
+        return self.out
+
+    def step_native(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, emit_lo: bool = True,
+                    phase_events=None):
+        """The same decode step as :meth:`step`, launched by one native call."""
+        self.length += 1
+        L = self.length
+        mikv_decode_step(self.cache, L, q, k_new, v_new, self.out, self.k_heavy(L), self.wl.window, self.probs_hi,
+                         self.probs_lo if emit_lo else None, self.balance, None,
+                         ATTN_ACCUMULATE if self.fused else 0, self.step_ws, phase_events)
         return self.out

@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 14
+    assert len(names) == 16
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)

@@ -182,3 +182,23 @@ def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
     torch.cuda.synchronize()
     assert int(c.status.item()) & mikv.DEVERR_HI_FULL
     assert c.n_hi.cpu().tolist() == [4, 4]
+
+
+@pytest.mark.parametrize("name", ["llama2_13b", "mistral_7b"])
+@pytest.mark.parametrize("fused", [False, True])
+def test_native_step_matches_call_sequence(name, fused):
+    """mikv_decode_step (one native call) leaves exactly the state that the
+    four separate calls leave, and the same outputs."""
+    _dev()
+    wl = workloads.small_workload(name, **SMALL[name])
+    steps = 5
+    run = Lockstep(wl, steps, fused=fused)
+    run.prefill()
+    other = mikv.MikvDecoder(wl, max_len=wl.context + steps, device="cuda", fused=fused)
+    other.prefill(run.k.cuda(), run.v.cuda(), run.sc.cuda(), run.qp.cuda() if run.qp is not None else None)
+    for t in range(steps):
+        run.step(t)
+        other.step_native(run.q[t].cuda(), run.kn[t].cuda(), run.vn[t].cuda())
+        torch.cuda.synchronize()
+        compare_state(other.cache, run.orc, tag=f"native step {t}")
+        np.testing.assert_array_equal(other.out.cpu().numpy(), run.dec.out.cpu().numpy())
