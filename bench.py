@@ -93,6 +93,40 @@ def cpu_baseline(wl, steps_inputs, budget_s: float):
             "s_per_step_per_head": round(el / max(done, 1) / len(heads), 4)}
 
 
+def copy_probe(mb: int):
+    """Time a plain device-to-device copy of `mb` MB (read + write bytes):
+    the reference for achievable HBM bandwidth and for scaling PMC counters."""
+    import torch
+    n = mb * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    reps = 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    x = src.view(torch.int32)
+    for _ in range(3):
+        x.sum(dtype=torch.int64)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        x.sum(dtype=torch.int64)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_r = e0.elapsed_time(e1) / reps
+    rec = {"copy_probe_MB": mb, "ms_per_copy": round(ms, 4), "copy_read_plus_write_GBps": round(2 * n / ms / 1e6, 1),
+           "ms_per_sum": round(ms_r, 4), "sum_read_GBps": round(n / ms_r / 1e6, 1)}
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -102,6 +136,10 @@ def main():
     ap.add_argument("--fused", type=int, default=1, help="fuse the importance update into attention (default 1)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="time budget of the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--override", action="append", default=[], metavar="FIELD=VALUE",
+                    help="change a workload field, e.g. ratio_num=0 (experiments; reported in config)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
+                    help="instead of the bench: time a plain device-to-device copy of MB megabytes")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -113,7 +151,13 @@ def main():
 
     from paper_2402_18096_amd import mikv, workloads
 
+    if args.copy_probe:
+        return copy_probe(args.copy_probe)
     wl = workloads.WORKLOADS[args.workload]
+    for ov in args.override:
+        key, val = ov.split("=", 1)
+        cur = getattr(wl, key)
+        wl = wl.with_(**{key: type(cur)(val) if not isinstance(cur, bool) else val in ("1", "true", "True")})
     dev = torch.device("cuda:0")
     n_total = args.warmup + args.steps
     t_setup = time.perf_counter()
@@ -206,6 +250,8 @@ def main():
                      "traffic": None},
         "cpu_baseline": cpu,
     }
+    if args.override:
+        rec["config"]["overrides"] = args.override
     print(json.dumps(rec), flush=True)
 
 

@@ -4,26 +4,50 @@
 // Split-K over the sequence: every block takes one contiguous chunk of one
 // pool of one (sequence, KV head) -- chunks are homogeneous in precision
 // (the pools are grouped by precision, which permutation invariance allows)
-// and sized by bytes, so the fp16/INT8 and INT2/INT4 chunks cost about the
-// same.  A block serves all G query heads of the KV group, so GQA loads K/V
-// once.  Lanes: LPT lanes per token, each owning CPL = 128/LPT contiguous
-// channels; a wave covers 64/LPT tokens per iteration with fully coalesced
-// loads of the packed rows.  Each lane keeps its own value sums, the running
-// maximum is wave-uniform (tile maxima via lane shuffles), and the lanes and
-// waves are merged once per chunk.  The partial phase writes per-chunk
-// (max, sum, value-sum) records and the raw scores; the finalize phase merges
-// the records exactly, turns scores into probabilities and, optionally, adds
-// them to the importance scores.
+// and sized by bytes, so fp16/INT8 and INT2/INT4 chunks cost about the same.
+// A block serves all G query heads of the KV group, so GQA loads K/V once.
+//
+// One wave per chunk (many small work units keep every CU streaming).
+// Lanes: LPT = 128/CPL lanes per token, each owning CPL contiguous channels
+// (CPL = 32, or 16 for G = 8); a wave covers 64/LPT tokens per tile and
+// UNROLL tiles per iteration.  Rows are read through buffer descriptors
+// spanning the head's occupied slots (reads past them return zero and are
+// masked), contiguous across the lanes of a tile.
+//
+// Inner loop, with every code c in [0, 2^N) of a group with scale alpha and
+// zero beta (Eq. 1, decoded value alpha*c + beta):
+//   score:  q . k = alpha * sum_c q_c code_c + beta * sum_c q_c
+//   value:  e * v = (e*alpha) * code + e*beta, the e*beta part summed apart.
+// Codes are turned into fp16 operands with one AND per two codes: a code c
+// placed in the mantissa bits of a zero-exponent half is the fp16 subnormal
+// c * 2^(s-24), s the code's bit offset inside the half (codes never reach
+// the exponent bits; offsets 10..15 are shifted down first).  Products with
+// such halves are exact in fp32, the 2^(s-24) factors are folded into the
+// query (key side, v_dot2_f32_f16) and into the final sums (value side,
+// fp32 fma with an fp16 operand).  fp16 rows are used as stored.
+//
+// Softmax: the running maximum is wave-uniform and only raised when a score
+// exceeds it by more than 2^8 in the exponential (checked with a ballot), so
+// the common tile needs no cross-lane max.  Scores are kept in log2 units.
+// The partial phase writes per-chunk (max, sum, value-sum) records and the
+// scores; the finalize phase merges the records exactly, turns scores into
+// probabilities and optionally adds them to the importance scores.
+#include <algorithm>
+
 #include "mikv_internal.h"
 
 namespace mikv {
 
 namespace {
 
-constexpr int kBlock = 256;
-constexpr int kWaves = kBlock / 64;
+constexpr int kBlock = 256;        // finalize / importance kernels
+constexpr int kWaves = 1;          // the partial kernel runs one wave per chunk
 constexpr int kRec = 2 + kHeadDim;  // (max, sum, value-sum[128]) per query head and chunk
 constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLazy = 8.0f;       // raise the running max only past this (log2 units)
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 struct AttnArgs {
   const uint8_t *hi_k, *hi_v;
@@ -35,7 +59,7 @@ struct AttnArgs {
   const uint16_t *q;
   const float *balance;
   float scale;
-  float *scores_hi, *scores_lo;  // [B*Hq, cap] raw scores (nullable)
+  float *scores_hi, *scores_lo;  // [B*Hq, cap] scores in log2 units (nullable)
   float *partials;               // [B*Hq, nc_hi + nc_lo, kRec]
   float *probs_hi, *probs_lo;    // outputs (nullable)
   float *acc;                    // hi_acc when accumulating (nullable)
@@ -44,222 +68,395 @@ struct AttnArgs {
   int chunk_hi, chunk_lo, nc_hi, nc_lo;
 };
 
-// Channels per lane for a GQA group of G query heads (keeps q and the value
-// sums of all G heads in registers: G * CPL <= 32).
-template <int G>
-struct LaneShape {
-  static constexpr int CPL = G == 1 ? 32 : (G == 2 ? 16 : (G == 4 ? 8 : 4));
-  static constexpr int LPT = kHeadDim / CPL;
-  static constexpr int TPW = 64 / LPT;  // tokens per wave iteration
-};
-
-// Raw storage of CPL channels of one token at BITS (16 = fp16).
-template <int BITS, int CPL>
-struct Seg {
-  static constexpr int kBytes = BITS == 16 ? CPL * 2 : CPL * BITS / 8;
-  static constexpr int kWords = kBytes >= 4 ? kBytes / 4 : 1;
-  uint32_t w[kWords];
-  uint32_t param;
-};
-
-template <int BITS, int CPL>
-__device__ inline void load_seg(Seg<BITS, CPL> &s, const uint8_t *rowbase, const uint32_t *parbase,
-                                int part, int group) {
-  constexpr int B = Seg<BITS, CPL>::kBytes;
-  const uint8_t *p = rowbase + part * B;
-  if constexpr (B >= 16) {
-#pragma unroll
-    for (int i = 0; i < B / 16; ++i) {
-      uint4 v = reinterpret_cast<const uint4 *>(p)[i];
-      s.w[4 * i] = v.x;
-      s.w[4 * i + 1] = v.y;
-      s.w[4 * i + 2] = v.z;
-      s.w[4 * i + 3] = v.w;
-    }
-  } else if constexpr (B == 8) {
-    uint2 v = *reinterpret_cast<const uint2 *>(p);
-    s.w[0] = v.x;
-    s.w[1] = v.y;
-  } else if constexpr (B == 4) {
-    s.w[0] = *reinterpret_cast<const uint32_t *>(p);
-  } else if constexpr (B == 2) {
-    s.w[0] = *reinterpret_cast<const uint16_t *>(p);
-  } else {
-    s.w[0] = *p;
-  }
-  if constexpr (BITS != 16) s.param = parbase[(part * CPL) / group];
-}
-
-// Decoded fp32 value of channel c of the segment: the fp16 value, or
-// alpha * code + beta (the product is exact, so fmaf rounds exactly once,
-// like the separate multiply and add of Eq. 1).
-template <int BITS, int CPL>
-__device__ inline float seg_value(const Seg<BITS, CPL> &s, int c, float a, float b) {
-  if constexpr (BITS == 16) {
-    return f16_to_f32((uint16_t)(s.w[c >> 1] >> (16 * (c & 1))));
-  } else {
-    uint32_t code = (s.w[(c * BITS) / 32] >> ((c * BITS) % 32)) & ((1u << BITS) - 1u);
-    return fmaf(a, (float)code, b);
-  }
-}
-
+// ---------------------------------------------------------------------------
+// Packed-row formats.  A lane's CPL channels are held as NP = CPL/2 fp16
+// pairs; pair p holds lane-local channels lo(p) and hi(p), scaled by
+// 2^(cls(p) - 24) for codes (exact fp16 subnormals), or the stored fp16
+// values for BITS == 16.
+// ---------------------------------------------------------------------------
 template <int BITS>
-__device__ inline void seg_params(uint32_t param, float &a, float &b) {
-  if constexpr (BITS == 16) {
-    a = 1.0f;
-    b = 0.0f;
+struct Fmt {
+  static constexpr bool kQuant = BITS != 16;
+  __host__ __device__ static constexpr int lo(int p) {
+    return BITS == 16 ? 2 * p
+         : BITS == 8  ? 4 * (p / 2) + p % 2
+         : BITS == 4  ? 8 * (p / 4) + p % 4
+                      : 16 * (p / 8) + p % 8;
+  }
+  __host__ __device__ static constexpr int hi(int p) {
+    return BITS == 16 ? 2 * p + 1 : lo(p) + (BITS == 8 ? 2 : BITS == 4 ? 4 : 8);
+  }
+  __host__ __device__ static constexpr int cls(int p) {
+    return BITS == 4 ? 4 * (p % 2) : BITS == 2 ? 2 * (p % 4) : 0;
+  }
+  template <int CPL>
+  __device__ static inline void unpack(const uint32_t *raw, uint32_t *out) {
+    if constexpr (BITS == 16) {
+#pragma unroll
+      for (int j = 0; j < CPL / 2; ++j) out[j] = raw[j];
+    } else if constexpr (BITS == 8) {
+#pragma unroll
+      for (int j = 0; j < CPL / 4; ++j) {
+        out[2 * j] = raw[j] & 0x00ff00ffu;
+        out[2 * j + 1] = (raw[j] >> 8) & 0x00ff00ffu;
+      }
+    } else if constexpr (BITS == 4) {
+#pragma unroll
+      for (int j = 0; j < CPL / 8; ++j) {
+        const uint32_t x = raw[j], y = x >> 8;
+        out[4 * j] = x & 0x000f000fu;
+        out[4 * j + 1] = x & 0x00f000f0u;
+        out[4 * j + 2] = y & 0x000f000fu;
+        out[4 * j + 3] = y & 0x00f000f0u;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < CPL / 16; ++j) {
+        const uint32_t x = raw[j], y = x >> 8;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          out[8 * j + k] = x & (0x00030003u << (2 * k));
+          out[8 * j + 4 + k] = y & (0x00030003u << (2 * k));
+        }
+      }
+    }
+  }
+};
+
+__device__ inline half2_t as_h2(uint32_t u) { return __builtin_bit_cast(half2_t, u); }
+
+// Sum over the LPT consecutive lanes of a token (LPT = 4 or 8).
+template <int LPT>
+__device__ inline float token_sum(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, true));
+  if constexpr (LPT == 8)  // other quad of the half-row
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xF, 0xF, true));
+  return v;
+}
+
+// Sum over the 64/LPT lanes that hold the same `part` (same channels,
+// different tokens): rotations inside each 16-lane row, shuffles across rows.
+template <int LPT>
+__device__ inline float sum_token_lanes(float v) {
+  if constexpr (LPT == 4) {
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x124, 0xF, 0xF, false));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));
   } else {
-    a = f16_to_f32((uint16_t)(param & 0xffffu));
-    b = f16_to_f32((uint16_t)(param >> 16));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));
+  }
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
+  return v;
+}
+
+template <int BITS, int CPL>
+struct Rows {
+  static constexpr int KW = BITS == 16 ? CPL / 2 : CPL * BITS / 32;  // raw dwords per row segment
+  uint32_t k[KW], v[KW];
+  uint32_t kp, vp;
+};
+
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRsrcFlags = 0x00020000;  // raw (untyped) buffer, gfx9 descriptor word 3
+
+// A buffer resource over `bytes` bytes at `base`: loads at offsets past the
+// end return zero (so reading past the occupied slots of a pool is safe).
+__device__ inline rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRsrcFlags);
+}
+
+// Load one token's row segments (this lane's channels) and group params at
+// byte offsets `orow` (rows) and `opar` (params) of the head's pools.
+template <int BITS, int CPL>
+__device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, rsrc_t rkp, rsrc_t rvp, uint32_t orow,
+                                     uint32_t opar) {
+  constexpr int KW = Rows<BITS, CPL>::KW;
+  if constexpr (KW >= 4) {
+#pragma unroll
+    for (int i = 0; i < KW / 4; ++i) {
+      auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, orow + 16 * i, 0, 0);
+      auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, orow + 16 * i, 0, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        r.k[4 * i + j] = a[j];
+        r.v[4 * i + j] = b[j];
+      }
+    }
+  } else if constexpr (KW == 2) {
+    auto a = __builtin_amdgcn_raw_buffer_load_b64(rk, orow, 0, 0);
+    auto b = __builtin_amdgcn_raw_buffer_load_b64(rv, orow, 0, 0);
+    r.k[0] = a[0]; r.k[1] = a[1];
+    r.v[0] = b[0]; r.v[1] = b[1];
+  } else {
+    r.k[0] = __builtin_amdgcn_raw_buffer_load_b32(rk, orow, 0, 0);
+    r.v[0] = __builtin_amdgcn_raw_buffer_load_b32(rv, orow, 0, 0);
+  }
+  if constexpr (BITS != 16) {
+    r.kp = __builtin_amdgcn_raw_buffer_load_b32(rkp, opar, 0, 0);
+    r.vp = __builtin_amdgcn_raw_buffer_load_b32(rvp, opar, 0, 0);
   }
 }
 
-template <int BITS, int G>
+template <int BITS, int G, int CPL, bool SPLITQ, int UNROLL, int PREFETCH>
 __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, bool is_hi) {
-  using S = LaneShape<G>;
-  constexpr int CPL = S::CPL, LPT = S::LPT, TPW = S::TPW;
+  using F = Fmt<BITS>;
+  constexpr int LPT = kHeadDim / CPL, TPW = 64 / LPT, NP = CPL / 2;
+  constexpr bool Q = F::kQuant;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int part = lane % LPT, tsub = lane / LPT;
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
-  const int qh0 = b * A.q_heads + kvh * G;  // first query head of the group
+  const int qh0 = b * A.q_heads + kvh * G;
 
   const int cap = is_hi ? A.cap_hi : A.cap_lo;
   const int chunk_len = is_hi ? A.chunk_hi : A.chunk_lo;
   const int n_pool = is_hi ? A.n_hi[h] : A.n_lo[h];
   const int start = chunk * chunk_len;
   const int end = min(start + chunk_len, n_pool);
-  const int64_t row_bytes = BITS == 16 ? kHeadDim * 2 : kHeadDim * BITS / 8;
+  constexpr int64_t kRow = BITS == 16 ? kHeadDim * 2 : kHeadDim * BITS / 8;
   const int ng = kHeadDim / A.group;
-  const uint8_t *kbase = (is_hi ? A.hi_k : A.lo_k) + (int64_t)h * cap * row_bytes;
-  const uint8_t *vbase = (is_hi ? A.hi_v : A.lo_v) + (int64_t)h * cap * row_bytes;
-  const uint32_t *kpbase = (is_hi ? A.hi_kp : A.lo_kp) + (int64_t)h * cap * ng;
-  const uint32_t *vpbase = (is_hi ? A.hi_vp : A.lo_vp) + (int64_t)h * cap * ng;
+  const uint8_t *kb = (is_hi ? A.hi_k : A.lo_k) + (int64_t)h * cap * kRow;
+  const uint8_t *vb = (is_hi ? A.hi_v : A.lo_v) + (int64_t)h * cap * kRow;
+  const uint32_t *kpb = Q ? (is_hi ? A.hi_kp : A.lo_kp) + (int64_t)h * cap * ng : nullptr;
+  const uint32_t *vpb = Q ? (is_hi ? A.hi_vp : A.lo_vp) + (int64_t)h * cap * ng : nullptr;
   float *scores = is_hi ? A.scores_hi : A.scores_lo;
+  const float s2scale = A.scale * kLog2e;
 
-  // q_hat = q / balance (Eq. 4), this lane's channels, all G heads.
-  float qr[G][CPL];
+  // Query (Eq. 4: q / balance), as fp16 pairs matching the format's pairing,
+  // each pair pre-scaled by 2^-cls; with SPLITQ a second fp16 pair carries
+  // the rounding remainder.  qsum = sum of the lane's query channels (fp32).
+  half2_t qh[G][NP], ql[G][SPLITQ ? NP : 1];
+  float qsum[G];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
+    const uint16_t *qrow = A.q + (int64_t)(qh0 + i) * kHeadDim + part * CPL;
+    const float *brow = A.balance ? A.balance + (int64_t)h * kHeadDim + part * CPL : nullptr;
+    auto qhat = [&](int c) {
+      float v = f16_to_f32(qrow[c]);
+      return brow ? v / brow[c] : v;
+    };
+    float s = 0.0f;
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      int ch = part * CPL + c;
-      float qv = f16_to_f32(A.q[(int64_t)(qh0 + i) * kHeadDim + ch]);
-      if (A.balance) qv = qv / A.balance[(int64_t)h * kHeadDim + ch];
-      qr[i][c] = qv;
+    for (int c = 0; c < CPL; ++c) s += qhat(c);
+    qsum[i] = s;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const float sc = __builtin_ldexpf(1.0f, -F::cls(p));
+      const float a = qhat(F::lo(p)) * sc, bb = qhat(F::hi(p)) * sc;
+      const _Float16 ah = (_Float16)a, bh = (_Float16)bb;
+      qh[i][p] = half2_t{ah, bh};
+      if constexpr (SPLITQ) ql[i][p] = half2_t{(_Float16)(a - (float)ah), (_Float16)(bb - (float)bh)};
     }
   }
 
-  float m[G], l[G], o[G][CPL];
+  float m2[G], l[G], bsum[G], o[G][CPL];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    m[i] = kNegInf;
+    m2[i] = kNegInf;
     l[i] = 0.0f;
+    bsum[i] = 0.0f;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) o[i][c] = 0.0f;
   }
 
-  for (int base = start; base < end; base += kWaves * TPW) {
-    const int tok = base + wave * TPW + tsub;
-    const bool valid = tok < end;
-    const int slot = valid ? tok : start;  // invalid lanes re-read a valid row
-    Seg<BITS, CPL> ks, vs;
-    load_seg<BITS, CPL>(ks, kbase + (int64_t)slot * row_bytes, kpbase + (int64_t)slot * ng, part, A.group);
-    load_seg<BITS, CPL>(vs, vbase + (int64_t)slot * row_bytes, vpbase + (int64_t)slot * ng, part, A.group);
-    float ka, kb, va, vb;
-    seg_params<BITS>(ks.param, ka, kb);
-    seg_params<BITS>(vs.param, va, vb);
+  constexpr int kPerIter = kWaves * TPW * UNROLL;
+  constexpr int kSeg = Rows<BITS, CPL>::KW * 4;  // bytes of one lane's row segment
+  const int n_iter = end > start ? (end - start + kPerIter - 1) / kPerIter : 0;
+  const int first = start + wave * TPW * UNROLL + tsub;  // this lane's token in iteration 0, u = 0
+  auto tok_of = [&](int it, int u) { return first + it * kPerIter + u * TPW; };
+  const int g_lane = (part * CPL) / A.group;
+  // Buffer resources over this head's occupied slots; a lane's offset is
+  // fixed per iteration and the unroll steps are immediate offsets.
+  const rsrc_t rk = make_rsrc(kb, (uint32_t)n_pool * (uint32_t)kRow);
+  const rsrc_t rv = make_rsrc(vb, (uint32_t)n_pool * (uint32_t)kRow);
+  const rsrc_t rkp = make_rsrc(Q ? (const void *)kpb : (const void *)kb, Q ? (uint32_t)n_pool * ng * 4u : 0u);
+  const rsrc_t rvp = make_rsrc(Q ? (const void *)vpb : (const void *)vb, Q ? (uint32_t)n_pool * ng * 4u : 0u);
+  const uint32_t lane_tok = (uint32_t)(start + wave * TPW * UNROLL + tsub);
+  const uint32_t off_row0 = lane_tok * (uint32_t)kRow + (uint32_t)(part * kSeg);
+  const uint32_t off_par0 = (lane_tok * (uint32_t)ng + (uint32_t)g_lane) * 4u;
 
-    float s[G];
+  auto load_it = [&](Rows<BITS, CPL>(&r)[UNROLL], int it) {
+    const uint32_t orow = off_row0 + (uint32_t)(it * kPerIter) * (uint32_t)kRow;
+    const uint32_t opar = off_par0 + (uint32_t)(it * kPerIter) * (uint32_t)ng * 4u;
 #pragma unroll
-    for (int i = 0; i < G; ++i) s[i] = 0.0f;
+    for (int u = 0; u < UNROLL; ++u)
+      load_seg_rows<BITS, CPL>(r[u], rk, rv, rkp, rvp, orow + (uint32_t)(u * TPW * kRow),
+                               opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u);
+  };
+
+  float *score_row[G];
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      float kv = seg_value<BITS, CPL>(ks, c, ka, kb);
+  for (int i = 0; i < G; ++i) score_row[i] = scores ? scores + (int64_t)(qh0 + i) * cap : nullptr;
+
+  auto proc = [&](Rows<BITS, CPL>(&cur)[UNROLL], int it) {
+    float s2[UNROLL][G];
+    bool valid[UNROLL];
+    bool raise = false;
 #pragma unroll
-      for (int i = 0; i < G; ++i) s[i] = fmaf(qr[i][c], kv, s[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < G; ++i) {
-      s[i] = sum_lanes<LPT>(s[i]) * A.scale;
-      if (!valid) s[i] = kNegInf;
-      if (scores && valid && part == 0) scores[(int64_t)(qh0 + i) * cap + tok] = s[i];
-      float tmax = wave_max(s[i]);
-      if (tmax > m[i]) {
-        float f = m[i] == kNegInf ? 0.0f : __expf(m[i] - tmax);
-        l[i] *= f;
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) o[i][c] *= f;
-        m[i] = tmax;
+    for (int u = 0; u < UNROLL; ++u) {
+      const int t = tok_of(it, u);
+      valid[u] = t < end;
+      uint32_t kx[NP];
+      F::template unpack<CPL>(cur[u].k, kx);
+      float ka = 1.0f, kbeta = 0.0f;
+      if constexpr (Q) {
+        ka = __builtin_ldexpf(f16_to_f32((uint16_t)(cur[u].kp & 0xffffu)), 24);
+        kbeta = f16_to_f32((uint16_t)(cur[u].kp >> 16));
       }
-      s[i] = valid ? __expf(s[i] - m[i]) : 0.0f;
-      if (part == 0) l[i] += s[i];
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        float d = 0.0f;
+#pragma unroll
+        for (int p = 0; p < NP; ++p) d = __builtin_amdgcn_fdot2(as_h2(kx[p]), qh[i][p], d, false);
+        if constexpr (SPLITQ) {
+#pragma unroll
+          for (int p = 0; p < NP; ++p) d = __builtin_amdgcn_fdot2(as_h2(kx[p]), ql[i][p], d, false);
+        }
+        float s = Q ? fmaf(ka, d, kbeta * qsum[i]) : d;
+        s = token_sum<LPT>(s) * s2scale;
+        s = valid[u] ? s : kNegInf;
+        s2[u][i] = s;
+        if (scores && valid[u] && part == 0) score_row[i][t] = s;
+        raise = raise || (s > m2[i] + kLazy);
+      }
+    }
+    if (__ballot(raise)) {
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        float mx = s2[0][i];
+#pragma unroll
+        for (int u = 1; u < UNROLL; ++u) mx = fmaxf(mx, s2[u][i]);
+        mx = wave_max(mx);
+        if (mx > m2[i]) {
+          const float f = m2[i] == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(m2[i] - mx);
+          l[i] *= f;
+          bsum[i] *= f;
+#pragma unroll
+          for (int c = 0; c < CPL; ++c) o[i][c] *= f;
+          m2[i] = mx;
+        }
+      }
     }
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      float vv = seg_value<BITS, CPL>(vs, c, va, vb);
+    for (int u = 0; u < UNROLL; ++u) {
+      uint32_t vx[NP];
+      F::template unpack<CPL>(cur[u].v, vx);
+      float va = 1.0f, vbeta = 0.0f;
+      if constexpr (Q) {
+        va = f16_to_f32((uint16_t)(cur[u].vp & 0xffffu));
+        vbeta = f16_to_f32((uint16_t)(cur[u].vp >> 16));
+      }
 #pragma unroll
-      for (int i = 0; i < G; ++i) o[i][c] = fmaf(s[i], vv, o[i][c]);
+      for (int i = 0; i < G; ++i) {
+        const float e = valid[u] ? __builtin_amdgcn_exp2f(s2[u][i] - m2[i]) : 0.0f;
+        l[i] += e;
+        const float w = Q ? e * va : e;
+        if constexpr (Q) bsum[i] = fmaf(e, vbeta, bsum[i]);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const half2_t hv = as_h2(vx[p]);
+          o[i][F::lo(p)] = fmaf(w, (float)hv.x, o[i][F::lo(p)]);
+          o[i][F::hi(p)] = fmaf(w, (float)hv.y, o[i][F::hi(p)]);
+        }
+      }
+    }
+  };
+
+  // Software pipeline: the rows of the next PREFETCH iterations are loaded
+  // while the current one is computed.
+  Rows<BITS, CPL> cur[UNROLL];
+  if constexpr (PREFETCH == 0) {
+    for (int it = 0; it < n_iter; ++it) {
+      load_it(cur, it);
+      proc(cur, it);
+    }
+  } else if constexpr (PREFETCH == 1) {
+    Rows<BITS, CPL> n1[UNROLL];
+    if (n_iter > 0) load_it(cur, 0);
+    for (int it = 0; it < n_iter; ++it) {
+      if (it + 1 < n_iter) load_it(n1, it + 1);
+      proc(cur, it);
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) cur[u] = n1[u];
+    }
+  } else {
+    Rows<BITS, CPL> n1[UNROLL], n2[UNROLL];
+    if (n_iter > 0) load_it(cur, 0);
+    if (n_iter > 1) load_it(n1, 1);
+    for (int it = 0; it < n_iter; ++it) {
+      if (it + 2 < n_iter) load_it(n2, it + 2);
+      proc(cur, it);
+#pragma unroll
+      for (int u = 0; u < UNROLL; ++u) {
+        cur[u] = n1[u];
+        n1[u] = n2[u];
+      }
     }
   }
 
-  // merge lanes of equal `part` (same channels), then waves through LDS
+  // Undo the code scaling, add the beta part, merge the lanes of equal
+  // `part` (same channels), and write this chunk's record.
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    l[i] = wave_sum(l[i]);
+    if constexpr (Q) {
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-#pragma unroll
-      for (int off = LPT; off < 64; off <<= 1) o[i][c] += __shfl_xor(o[i][c], off, 64);
-    }
-  }
-  __shared__ float s_m[kWaves][G], s_l[kWaves][G];
-  __shared__ float s_o[kWaves][G][kHeadDim];
-  if (lane == 0) {
-#pragma unroll
-    for (int i = 0; i < G; ++i) {
-      s_m[wave][i] = m[i];
-      s_l[wave][i] = l[i];
-    }
-  }
-  if (tsub == 0) {
-#pragma unroll
-    for (int i = 0; i < G; ++i)
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) s_o[wave][i][part * CPL + c] = o[i][c];
-  }
-  __syncthreads();
-  const int nc = A.nc_hi + A.nc_lo;
-  for (int idx = threadIdx.x; idx < G * kRec; idx += kBlock) {
-    const int i = idx / kRec, e = idx % kRec;
-    float M = kNegInf;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, s_m[w][i]);
-    float val = 0.0f;
-    if (e == 0) {
-      val = M;
-    } else {
-#pragma unroll
-      for (int w = 0; w < kWaves; ++w) {
-        float f = s_m[w][i] == kNegInf ? 0.0f : __expf(s_m[w][i] - M);
-        val += f * (e == 1 ? s_l[w][i] : s_o[w][i][e - 2]);
+      for (int p = 0; p < NP; ++p) {
+        const float sc = __builtin_ldexpf(1.0f, 24 - F::cls(p));
+        o[i][F::lo(p)] = fmaf(o[i][F::lo(p)], sc, bsum[i]);
+        o[i][F::hi(p)] = fmaf(o[i][F::hi(p)], sc, bsum[i]);
       }
     }
-    A.partials[((int64_t)(qh0 + i) * nc + rec_chunk) * kRec + e] = val;
+    l[i] = wave_sum(l[i]) * (1.0f / LPT);  // every lane of a token added its e
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) o[i][c] = sum_token_lanes<LPT>(o[i][c]);
+  }
+  const int nc = A.nc_hi + A.nc_lo;
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    float *rec = A.partials + ((int64_t)(qh0 + i) * nc + rec_chunk) * kRec;
+    if (lane == 0) {
+      rec[0] = m2[i];
+      rec[1] = l[i];
+    }
+    if (tsub == 0) {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) rec[2 + part * CPL + c] = o[i][c];
+    }
   }
 }
 
-template <int HI, int LO, int G>
-__global__ __launch_bounds__(kBlock) void attn_partial_kernel(AttnArgs A) {
+// Tuning: token tiles per lane per iteration and prefetch depth, for
+// low-bit (INT2/INT4) and high-bit (fp16/INT8) rows.
+#ifndef MIKV_UNROLL_LOWBIT
+#define MIKV_UNROLL_LOWBIT 8
+#endif
+#ifndef MIKV_UNROLL_HIGHBIT
+#define MIKV_UNROLL_HIGHBIT 1
+#endif
+#ifndef MIKV_PREFETCH_LOWBIT
+#define MIKV_PREFETCH_LOWBIT 0
+#endif
+#ifndef MIKV_PREFETCH_HIGHBIT
+#define MIKV_PREFETCH_HIGHBIT 1
+#endif
+template <int BITS>
+constexpr int unroll_for() { return BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL_HIGHBIT; }
+template <int BITS>
+constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PREFETCH_HIGHBIT; }
+
+template <int HI, int LO, int G, bool SPLITQ>
+__global__ __launch_bounds__(64) void attn_partial_kernel(AttnArgs A) {
+  constexpr int CPL = G == 8 ? 16 : 32;
   const int h = blockIdx.y, c = blockIdx.x;
   if (c < A.nc_hi)
-    attn_chunk<HI, G>(A, h, c, c, true);
+    attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true);
   else
-    attn_chunk<LO, G>(A, h, c - A.nc_hi, c, false);
+    attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false);
 }
 
 // Merge the chunk records of every query head of KV head h; turn this
-// block's chunk of raw scores into probabilities (and optionally add them to
-// the importance scores); block 0 of each head also writes the output.
+// block's chunk of scores into probabilities (and optionally add them to the
+// importance scores); block 0 of each head also writes the output.
 template <int G>
 __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int accumulate) {
   const int h = blockIdx.y, c = blockIdx.x;
@@ -267,7 +464,7 @@ __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int a
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
-  __shared__ float s_M[G], s_L[G];
+  __shared__ float s_M[G], s_inv[G];
   for (int i = wave; i < G; i += kWaves) {
     const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
     float M = kNegInf;
@@ -275,13 +472,13 @@ __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int a
     M = wave_max(M);
     float L = 0.0f;
     for (int r = lane; r < nc; r += 64) {
-      float mr = rec[(int64_t)r * kRec];
-      if (mr != kNegInf) L += rec[(int64_t)r * kRec + 1] * __expf(mr - M);
+      const float mr = rec[(int64_t)r * kRec];
+      if (mr != kNegInf) L = fmaf(rec[(int64_t)r * kRec + 1], __builtin_amdgcn_exp2f(mr - M), L);
     }
     L = wave_sum(L);
     if (lane == 0) {
       s_M[i] = M;
-      s_L[i] = L;
+      s_inv[i] = 1.0f / L;
     }
   }
   __syncthreads();
@@ -300,7 +497,7 @@ __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int a
       float sum = 0.0f;
 #pragma unroll
       for (int i = 0; i < G; ++i) {
-        float p = __expf(scores[(int64_t)(qh0 + i) * cap + t] - s_M[i]) / s_L[i];
+        const float p = __builtin_amdgcn_exp2f(scores[(int64_t)(qh0 + i) * cap + t] - s_M[i]) * s_inv[i];
         if (probs) probs[(int64_t)(qh0 + i) * cap + t] = p;
         sum = i == 0 ? p : sum + p;
       }
@@ -313,10 +510,10 @@ __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int a
       const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
       float v = 0.0f;
       for (int r = 0; r < nc; ++r) {
-        float mr = rec[(int64_t)r * kRec];
-        if (mr != kNegInf) v += rec[(int64_t)r * kRec + 2 + d] * __expf(mr - s_M[i]);
+        const float mr = rec[(int64_t)r * kRec];
+        if (mr != kNegInf) v = fmaf(rec[(int64_t)r * kRec + 2 + d], __builtin_amdgcn_exp2f(mr - s_M[i]), v);
       }
-      A.out[(int64_t)(qh0 + i) * kHeadDim + d] = v / s_L[i];
+      A.out[(int64_t)(qh0 + i) * kHeadDim + d] = v * s_inv[i];
     }
   }
 }
@@ -350,11 +547,12 @@ Plan make_plan(const mikv_cache *c, int length) {
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int64_t bh = token_bytes(c->hi_bits, c->group), bl = token_bytes(c->lo_bits, c->group);
   const int64_t total = NH * (span_hi * bh + span_lo * bl);
-  // Aim for ~8 blocks per CU over 256 CUs, at least 32 KiB and at most
-  // 512 KiB of packed K/V per block.
-  int64_t target = std::min<int64_t>(std::max<int64_t>(total / 2048, 32 << 10), 512 << 10);
-  p.chunk_hi = std::max(64, round_up(target / bh, 64));
-  p.chunk_lo = std::max(64, round_up(target / bl, 64));
+  // One wave per chunk; ~96 KiB of packed K/V per chunk (many small work
+  // units balance the CUs best), at least 16 KiB so the per-chunk merge
+  // stays cheap.  Chunks are whole wave iterations (128 tokens).
+  int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, 96 << 10), 16 << 10);
+  p.chunk_hi = std::max(128, round_up(target / bh, 128));
+  p.chunk_lo = std::max(128, round_up(target / bl, 128));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
   p.nc_lo = std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
   return p;
@@ -403,14 +601,24 @@ AttnArgs make_args(const mikv_cache *c, const Plan &p, const uint16_t *q, const 
   return A;
 }
 
+template <int HI, int LO, bool SPLITQ>
+void launch_partial_q(const AttnArgs &A, int G, dim3 grid, hipStream_t st) {
+  switch (G) {
+    case 1: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 1, SPLITQ>), grid, dim3(64), 0, st, A); break;
+    case 2: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 2, SPLITQ>), grid, dim3(64), 0, st, A); break;
+    case 4: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 4, SPLITQ>), grid, dim3(64), 0, st, A); break;
+    default: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 8, SPLITQ>), grid, dim3(64), 0, st, A); break;
+  }
+}
+
+// A balanced query (q / b) is not an fp16 value in general: carry it as two
+// fp16 parts.  An unbalanced query is fp16 already.
 template <int HI, int LO>
 void launch_partial_g(const AttnArgs &A, int G, dim3 grid, hipStream_t st) {
-  switch (G) {
-    case 1: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 1>), grid, dim3(kBlock), 0, st, A); break;
-    case 2: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 2>), grid, dim3(kBlock), 0, st, A); break;
-    case 4: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 4>), grid, dim3(kBlock), 0, st, A); break;
-    default: hipLaunchKernelGGL((attn_partial_kernel<HI, LO, 8>), grid, dim3(kBlock), 0, st, A); break;
-  }
+  if (A.balance)
+    launch_partial_q<HI, LO, true>(A, G, grid, st);
+  else
+    launch_partial_q<HI, LO, false>(A, G, grid, st);
 }
 
 int check_attention_args(const mikv_cache *c, int32_t length, const uint16_t *q, float *out, void *ws,

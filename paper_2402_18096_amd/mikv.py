@@ -21,7 +21,8 @@ from typing import Optional
 
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmikv.so")
+# MIKV_LIB selects another build of the library (e.g. to compare builds).
+LIB_PATH = os.environ.get("MIKV_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmikv.so")
 HEAD_DIM = 128
 ATTN_ACCUMULATE = 1
 DEVERR_HI_FULL = 1
