@@ -42,7 +42,10 @@ namespace {
 
 constexpr int kBlock = 256;        // finalize / importance kernels
 constexpr int kWaves = 1;          // the partial kernel runs one wave per chunk
-constexpr int kRec = 2 + kHeadDim;  // (max, sum, value-sum[128]) per query head and chunk
+// Chunk record per query head and chunk: max, sum, two pad words, value
+// sum[128] (kept 16-byte aligned for vector loads).
+constexpr int kRecO = 4;
+constexpr int kRec = kRecO + kHeadDim;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLazy = 8.0f;       // raise the running max only past this (log2 units)
@@ -419,8 +422,10 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
       rec[1] = l[i];
     }
     if (tsub == 0) {
+      float4 *r4 = reinterpret_cast<float4 *>(rec + kRecO + part * CPL);
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) rec[2 + part * CPL + c] = o[i][c];
+      for (int c = 0; c < CPL / 4; ++c)
+        r4[c] = make_float4(o[i][4 * c], o[i][4 * c + 1], o[i][4 * c + 2], o[i][4 * c + 3]);
     }
   }
 }
@@ -454,67 +459,120 @@ __global__ __launch_bounds__(64) void attn_partial_kernel(AttnArgs A) {
     attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false);
 }
 
-// Merge the chunk records of every query head of KV head h; turn this
-// block's chunk of scores into probabilities (and optionally add them to the
-// importance scores); block 0 of each head also writes the output.
+// Softmax over the whole sequence from the chunk records (Section 2.1): a
+// query head's max M is the largest chunk max, its normaliser L the chunk
+// sums rescaled by exp2(m_r - M); the output is the rescaled value sums / L.
+// Every block derives (M, 1/L) of the G query heads of KV head h from the
+// (m, l) pairs, then turns one tile of scores into probabilities (and adds
+// their GQA sum to the importance scores when asked); block 0 also merges
+// the value sums into the output.
+constexpr int kProbTile = 2 * kBlock;  // scores per block and query head
+
+template <int W>
+__device__ inline float max_lanes(float v) {
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
 template <int G>
-__global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int accumulate) {
+__global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi,
+                                                               int tiles_lo) {
+  constexpr int TPH = G <= 4 ? 64 : 32;  // lanes per query head for the statistics
   const int h = blockIdx.y, c = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
   __shared__ float s_M[G], s_inv[G];
-  for (int i = wave; i < G; i += kWaves) {
-    const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
-    float M = kNegInf;
-    for (int r = lane; r < nc; r += 64) M = fmaxf(M, rec[(int64_t)r * kRec]);
-    M = wave_max(M);
-    float L = 0.0f;
-    for (int r = lane; r < nc; r += 64) {
-      const float mr = rec[(int64_t)r * kRec];
-      if (mr != kNegInf) L = fmaf(rec[(int64_t)r * kRec + 1], __builtin_amdgcn_exp2f(mr - M), L);
+  {
+    const int i = threadIdx.x / TPH, r0 = threadIdx.x % TPH;
+    float m = kNegInf, l = 0.0f;
+    if (i < G) {
+      const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
+      for (int r = r0; r < nc; r += TPH) {
+        const float2 ml = *reinterpret_cast<const float2 *>(rec + (int64_t)r * kRec);
+        if (ml.x > m) {
+          l = fmaf(l, __builtin_amdgcn_exp2f(m - ml.x), ml.y);
+          m = ml.x;
+        } else if (ml.x != kNegInf) {
+          l = fmaf(ml.y, __builtin_amdgcn_exp2f(ml.x - m), l);
+        }
+      }
     }
-    L = wave_sum(L);
-    if (lane == 0) {
+    const float M = max_lanes<TPH>(m);
+    const float L = sum_lanes<TPH>(m == kNegInf ? 0.0f : l * __builtin_amdgcn_exp2f(m - M));
+    if (i < G && r0 == 0) {
       s_M[i] = M;
       s_inv[i] = 1.0f / L;
     }
   }
   __syncthreads();
 
-  const bool is_hi = c < A.nc_hi;
-  const int chunk = is_hi ? c : c - A.nc_hi;
-  const int chunk_len = is_hi ? A.chunk_hi : A.chunk_lo;
+  if (c == 0) {
+    // Thread -> (record split s, query head i, 4 channels q4).
+    constexpr int S = 8 / G;
+    const int q4 = threadIdx.x % 32, i = (threadIdx.x / 32) % G, s = threadIdx.x / (32 * G);
+    const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
+    const float Mi = s_M[i];
+    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll 4
+    for (int r = s; r < nc; r += S) {
+      const float *rr = rec + (int64_t)r * kRec;
+      const float mr = rr[0];
+      const float4 o = reinterpret_cast<const float4 *>(rr + kRecO)[q4];
+      const float w = mr == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(mr - Mi);
+      v.x = fmaf(o.x, w, v.x);
+      v.y = fmaf(o.y, w, v.y);
+      v.z = fmaf(o.z, w, v.z);
+      v.w = fmaf(o.w, w, v.w);
+    }
+    __shared__ float4 s_o[kBlock];
+    s_o[threadIdx.x] = v;
+    __syncthreads();
+    if (s == 0) {
+      for (int s2 = 1; s2 < S; ++s2) {
+        const float4 u = s_o[threadIdx.x + s2 * 32 * G];
+        v.x += u.x;
+        v.y += u.y;
+        v.z += u.z;
+        v.w += u.w;
+      }
+      const float inv = s_inv[i];
+      reinterpret_cast<float4 *>(A.out + (int64_t)(qh0 + i) * kHeadDim)[q4] =
+          make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv);
+    }
+  }
+
+  const bool is_hi = c < tiles_hi;
+  if (!is_hi && c - tiles_hi >= tiles_lo) return;
+  const int tile = is_hi ? c : c - tiles_hi;
   const int n_pool = is_hi ? A.n_hi[h] : A.n_lo[h];
   const int cap = is_hi ? A.cap_hi : A.cap_lo;
   const float *scores = is_hi ? A.scores_hi : A.scores_lo;
   float *probs = is_hi ? A.probs_hi : A.probs_lo;
-  const bool acc = is_hi && accumulate && A.acc;
-  if (scores && (probs || acc)) {
-    const int start = chunk * chunk_len, end = min(start + chunk_len, n_pool);
-    for (int t = start + threadIdx.x; t < end; t += kBlock) {
-      float sum = 0.0f;
+  float *acc = is_hi && accumulate ? A.acc : nullptr;
+  constexpr int kPer = kProbTile / kBlock;
+  float sv[kPer][G], a[kPer];
+  int t[kPer];
 #pragma unroll
-      for (int i = 0; i < G; ++i) {
-        const float p = __builtin_amdgcn_exp2f(scores[(int64_t)(qh0 + i) * cap + t] - s_M[i]) * s_inv[i];
-        if (probs) probs[(int64_t)(qh0 + i) * cap + t] = p;
-        sum = i == 0 ? p : sum + p;
-      }
-      if (acc) A.acc[(int64_t)h * A.cap_hi + t] += sum;
-    }
+  for (int u = 0; u < kPer; ++u) {
+    t[u] = tile * kProbTile + u * kBlock + threadIdx.x;
+    const bool ok = t[u] < n_pool;
+#pragma unroll
+    for (int i = 0; i < G; ++i) sv[u][i] = ok ? scores[(int64_t)(qh0 + i) * cap + t[u]] : 0.0f;
+    a[u] = ok && acc ? acc[(int64_t)h * A.cap_hi + t[u]] : 0.0f;
   }
-  if (c == 0) {
-    for (int idx = threadIdx.x; idx < G * kHeadDim; idx += kBlock) {
-      const int i = idx / kHeadDim, d = idx % kHeadDim;
-      const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
-      float v = 0.0f;
-      for (int r = 0; r < nc; ++r) {
-        const float mr = rec[(int64_t)r * kRec];
-        if (mr != kNegInf) v = fmaf(rec[(int64_t)r * kRec + 2 + d], __builtin_amdgcn_exp2f(mr - s_M[i]), v);
-      }
-      A.out[(int64_t)(qh0 + i) * kHeadDim + d] = v * s_inv[i];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    if (t[u] >= n_pool) continue;
+    float sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      const float p = __builtin_amdgcn_exp2f(sv[u][i] - s_M[i]) * s_inv[i];
+      if (probs) probs[(int64_t)(qh0 + i) * cap + t[u]] = p;
+      sum = i == 0 ? p : sum + p;
     }
+    if (acc) acc[(int64_t)h * A.cap_hi + t[u]] = a[u] + sum;
   }
 }
 
@@ -675,14 +733,19 @@ extern "C" int mikv_decode_attention_finalize(const mikv_cache *c, int32_t lengt
   if (rc) return rc;
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, flags, ws);
-  dim3 grid(p.nc_hi + p.nc_lo, n_heads_of(c));
   hipStream_t st = (hipStream_t)stream;
   const int acc = (flags & MIKV_ATTN_ACCUMULATE) ? 1 : 0;
+  // probability tiles: importance pool when its probabilities are emitted or
+  // accumulated, retained pool when its probabilities are emitted
+  const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
+  const int tiles_hi = (A.scores_hi && (A.probs_hi || A.acc)) ? (span_hi + kProbTile - 1) / kProbTile : 0;
+  const int tiles_lo = A.probs_lo ? (span_lo + kProbTile - 1) / kProbTile : 0;
+  dim3 grid(std::max(1, tiles_hi + tiles_lo), n_heads_of(c));
   switch (group_size_of(c)) {
-    case 1: hipLaunchKernelGGL(attn_finalize_kernel<1>, grid, dim3(kBlock), 0, st, A, acc); break;
-    case 2: hipLaunchKernelGGL(attn_finalize_kernel<2>, grid, dim3(kBlock), 0, st, A, acc); break;
-    case 4: hipLaunchKernelGGL(attn_finalize_kernel<4>, grid, dim3(kBlock), 0, st, A, acc); break;
-    default: hipLaunchKernelGGL(attn_finalize_kernel<8>, grid, dim3(kBlock), 0, st, A, acc); break;
+    case 1: hipLaunchKernelGGL(attn_finalize_kernel<1>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;
+    case 2: hipLaunchKernelGGL(attn_finalize_kernel<2>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;
+    case 4: hipLaunchKernelGGL(attn_finalize_kernel<4>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;
+    default: hipLaunchKernelGGL(attn_finalize_kernel<8>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;
   }
   return check_launch("mikv_decode_attention_finalize");
 }

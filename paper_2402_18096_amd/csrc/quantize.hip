@@ -269,6 +269,52 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
   }
 }
 
+// One new token per head into the importance pool (the decoding step):
+// 8 lanes per head, lanes 0-3 the key row, 4-7 the value row.  The slot
+// count and the rows are loaded together; lane 0 of the head records the
+// position, the initial score and the map entry, and advances n_hi.
+template <int HI_BITS>
+__global__ __launch_bounds__(64) void append_one_kernel(Pools P, const uint16_t *k, const uint16_t *v,
+                                                        const float *balance, int pos, const float *score_init,
+                                                        int n_heads) {
+  const int t = blockIdx.x * 64 + threadIdx.x;
+  const int h = t >> 3;
+  if (h >= n_heads) return;  // all 8 lanes of a head leave together
+  const int is_v = (t >> 2) & 1, lane4 = t & 3;
+  const int n0 = P.n_hi[h];
+  const float *bal = (!is_v && balance) ? balance + (int64_t)h * kHeadDim + lane4 * 32 : nullptr;
+  float x[32];
+  load_row_segment((is_v ? v : k) + (int64_t)h * kHeadDim + lane4 * 32, bal, x);
+  const bool store = n0 < P.cap_hi;
+  const int64_t slot = (int64_t)h * P.cap_hi + (store ? n0 : 0);
+  if (HI_BITS == 16) {
+    if (store) {
+      uint32_t w[16];
+#pragma unroll
+      for (int c = 0; c < 16; ++c)
+        w[c] = (uint32_t)f32_to_f16_rne(x[2 * c]) | ((uint32_t)f32_to_f16_rne(x[2 * c + 1]) << 16);
+      uint4 *d4 = reinterpret_cast<uint4 *>((is_v ? P.hi_v : P.hi_k) + (slot * kHeadDim + lane4 * 32) * 2);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) d4[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
+    }
+  } else {
+    const int ng = kHeadDim / P.group;
+    uint8_t *dst = (is_v ? P.hi_v : P.hi_k) + slot * kHeadDim + lane4 * 32;
+    uint32_t *par = (is_v ? P.hi_vp : P.hi_kp) + slot * ng + (lane4 * 32) / P.group;
+    quantize_segment<8>(x, P.group, lane4, dst, par, store);
+  }
+  if ((t & 7) == 0) {
+    if (store) {
+      P.hi_pos[slot] = pos;
+      P.hi_acc[slot] = score_init ? score_init[h] : 0.0f;
+      if (P.map) P.map[(int64_t)h * P.max_len + pos] = 1;
+      P.n_hi[h] = n0 + 1;
+    } else {
+      atomicOr(P.status, MIKV_DEVERR_HI_FULL);
+    }
+  }
+}
+
 // Advance n_hi/n_lo after a multi-chunk placement.
 __global__ void commit_counts_kernel(Pools P, int n_heads, int n, const int32_t *counts, int nchunks) {
   int h = blockIdx.x * blockDim.x + threadIdx.x;
@@ -289,6 +335,11 @@ void launch_place(const mikv_cache *c, const uint16_t *k, const uint16_t *v, con
                   int n, const uint8_t *hi_mask, const float *score_init, int32_t *counts, hipStream_t st) {
   Pools P = make_pools(c);
   int NH = n_heads_of(c);
+  if (n == 1 && !hi_mask) {
+    hipLaunchKernelGGL((append_one_kernel<HI_BITS>), dim3((NH * 8 + 63) / 64), dim3(64), 0, st, P, k, v, balance,
+                       pos0, score_init, NH);
+    return;
+  }
   int nchunks = (n + kChunk - 1) / kChunk;
   if (hi_mask) {
     hipLaunchKernelGGL(count_hi_kernel, dim3(nchunks, NH), dim3(kChunk), 0, st, hi_mask, n, nchunks, counts);

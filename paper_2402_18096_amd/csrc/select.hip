@@ -191,11 +191,60 @@ __device__ inline void store_lo_segment(const SelArgs &A, uint8_t *codes, uint32
   if ((part % (A.group / 32)) == 0) *par = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
 }
 
+// Requantize importance-pool slot `slot` (K and V rows) into retained-pool
+// slot `lslot`; threads [0, 8) of the block take part (4 lanes per row).
+template <int HI_BITS, int LO_BITS>
+__device__ inline void demote_row(const SelArgs &A, int h, int slot, int64_t lslot, int p) {
+  if (threadIdx.x >= 8) return;
+  const int ng = kHeadDim / A.group;
+  const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  const int64_t lrow = kHeadDim * LO_BITS / 8;
+  const int is_v = threadIdx.x >> 2, part = threadIdx.x & 3;
+  const uint8_t *rows = (is_v ? A.hi_v : A.hi_k) + (int64_t)h * A.cap_hi * hrow;
+  const uint32_t *pars = HI_BITS == 16 ? nullptr : (is_v ? A.hi_vp : A.hi_kp) + (int64_t)h * A.cap_hi * ng;
+  float x[32];
+  load_hi_segment<HI_BITS>(A, rows, pars, slot, part, x);
+  uint8_t *codes = (is_v ? A.lo_v : A.lo_k) + lslot * lrow + part * (32 * LO_BITS / 8);
+  uint32_t *par = (is_v ? A.lo_vp : A.lo_kp) + lslot * ng + (part * 32) / A.group;
+  store_lo_segment<LO_BITS>(A, codes, par, part, x, true);
+  if (threadIdx.x == 0) {
+    A.lo_pos[lslot] = p;
+    if (A.map) A.map[(int64_t)h * A.max_len + p] = 0;
+  }
+}
+
+// Move importance-pool slot src into slot dst (rows, position, score and,
+// for INT8 rows, the scale/zero words); the whole block takes part.
+template <int HI_BITS>
+__device__ inline void move_slot(const SelArgs &A, int h, int src, int dst, int p, float a) {
+  const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  constexpr int chunks = (HI_BITS == 16 ? 2 * kHeadDim : kHeadDim) / 16;
+  const int ng = kHeadDim / A.group;
+  if (threadIdx.x < 2 * chunks) {
+    uint8_t *base = (threadIdx.x < chunks ? A.hi_k : A.hi_v) + (int64_t)h * A.cap_hi * hrow;
+    const int ck = threadIdx.x % chunks;
+    reinterpret_cast<uint4 *>(base + (int64_t)dst * hrow)[ck] =
+        reinterpret_cast<const uint4 *>(base + (int64_t)src * hrow)[ck];
+  }
+  if (threadIdx.x == 0) {
+    A.hi_pos[(int64_t)h * A.cap_hi + dst] = p;
+    A.hi_acc[(int64_t)h * A.cap_hi + dst] = a;
+  }
+  if (HI_BITS == 8 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
+    const int g = (threadIdx.x - 64) % ng;
+    uint32_t *pp = threadIdx.x - 64 < ng ? A.hi_kp : A.hi_vp;
+    pp[((int64_t)h * A.cap_hi + dst) * ng + g] = pp[((int64_t)h * A.cap_hi + src) * ng + g];
+  }
+}
+
+constexpr int kSelItems = 16;  // importance-pool slots per thread held in registers
+
 template <int HI_BITS, int LO_BITS>
 __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
   const int h = blockIdx.x;
   __shared__ int s_tmp_i[kSel / 64];
   __shared__ uint64_t s_tmp_u[kSel / 64];
+  __shared__ int s_arg[3];
   const int n = A.n_hi[h];
   const int n_lo0 = A.n_lo[h];
   const int thr = A.length - A.window;  // positions >= thr are in the window
@@ -204,8 +253,31 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
   auto elig = [&](int i) { return pos[i] < thr; };
   auto key = [&](int i) { return rank_key(acc[i], pos[i]); };
 
-  int cnt = 0;
-  for (int i = threadIdx.x; i < n; i += kSel) cnt += elig(i) ? 1 : 0;
+  // One pass over the pool, kSel * kSelItems slots per round trip: count
+  // the eligible slots and keep the least important one.
+  int cnt = 0, arg = -1;
+  uint64_t mn = ~0ull;
+  for (int base = 0; base < n; base += kSel * kSelItems) {
+    int pv[kSelItems];
+    float av[kSelItems];
+#pragma unroll
+    for (int u = 0; u < kSelItems; ++u) {
+      const int i = base + u * kSel + threadIdx.x;
+      pv[u] = i < n ? pos[i] : thr;
+      av[u] = i < n ? acc[i] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < kSelItems; ++u) {
+      if (pv[u] < thr) {
+        ++cnt;
+        const uint64_t k = rank_key(av[u], pv[u]);
+        if (k < mn) {
+          mn = k;
+          arg = base + u * kSel + threadIdx.x;
+        }
+      }
+    }
+  }
   const int n_elig = block_sum_int(cnt, s_tmp_i);
   const int n_dem = n_elig - A.k_heavy;
   if (n_dem <= 0) return;
@@ -214,18 +286,33 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
     return;
   }
 
-  uint64_t cut;
   if (n_dem == 1) {
-    uint64_t mn = ~0ull;
-    for (int i = threadIdx.x; i < n; i += kSel)
-      if (elig(i)) {
-        uint64_t k = key(i);
-        mn = k < mn ? k : mn;
-      }
-    cut = block_min_u64(mn, s_tmp_u);
-  } else {
-    cut = radix_select(n, n_dem, elig, key);
+    // Steady state of decoding: the least important eligible token leaves;
+    // the last slot fills its hole.
+    const uint64_t cut = block_min_u64(mn, s_tmp_u);
+    if (arg >= 0 && mn == cut) {
+      s_arg[0] = arg;
+      s_arg[1] = pos[arg];
+    }
+    if (threadIdx.x == 0) {
+      s_arg[2] = pos[n - 1];
+      s_tmp_u[0] = __float_as_uint(acc[n - 1]);
+    }
+    __syncthreads();
+    const int slot = s_arg[0];
+    demote_row<HI_BITS, LO_BITS>(A, h, slot, (int64_t)h * A.cap_lo + n_lo0, s_arg[1]);
+    __syncthreads();
+    if (slot != n - 1) move_slot<HI_BITS>(A, h, n - 1, slot, s_arg[2], __uint_as_float((uint32_t)s_tmp_u[0]));
+    if (threadIdx.x == 0) {
+      A.n_hi[h] = n - 1;
+      A.n_lo[h] = n_lo0 + 1;
+    }
+    return;
   }
+
+  // General case (several tokens leave): radix select of the cut, then
+  // ordered compaction of the holes and of the survivors that fill them.
+  const uint64_t cut = radix_select(n, n_dem, elig, key);
   auto demoted = [&](int i) { return elig(i) && key(i) <= cut; };
 
   int32_t *dem_list = A.ws + (int64_t)h * 2 * A.cap_hi;
