@@ -94,6 +94,26 @@ def cpu_baseline(wl, steps_inputs, budget_s: float):
             "s_per_step_per_head": round(el / max(done, 1) / len(heads), 4)}
 
 
+def measured_traffic(workload: str):
+    """HBM bytes per attention partial launch from the committed rocprofv3
+    counter runs (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter
+    reads for a copy of known size), or None when there is no record for this
+    workload or the kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"attn_partial_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    h = hashlib.sha256()
+    for name in ("attention.hip", "mikv_internal.h"):
+        with open(os.path.join(ROOT, "paper_2402_18096_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    if rec.get("source_sha256") != h.hexdigest():
+        return None
+    return rec
+
+
 def copy_probe(mb: int):
     """Time a plain device-to-device copy of `mb` MB (read + write bytes):
     the reference for achievable HBM bandwidth and for scaling PMC counters."""
@@ -237,10 +257,17 @@ def main():
         # per-launch algorithmic bytes / per-launch duration, averaged as the
         # ratio of the sums (every step's launch counts by its own bytes)
         achieved = total_bytes / (sum(part_ms) * 1e-3) / 1e9
+        tr = measured_traffic(wl.name) if not args.override else None
         roofline = {"kernel": "attn_partial_kernel", "bound": "hbm", "achieved": round(achieved, 2),
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                    "traffic": None, "mean_launch_us": round(mean(part_ms) * 1e3, 2),
+                    "traffic": tr["read_bytes"] + tr["write_bytes"] if tr else None,
+                    "traffic_unit": "HBM bytes per launch (read + write, rocprofv3 FETCH_SIZE/WRITE_SIZE, "
+                                    "copy-calibrated)",
+                    "mean_launch_us": round(mean(part_ms) * 1e3, 2),
                     "algorithmic_bytes_per_launch": int(mean_bytes)}
+        if tr:
+            roofline["traffic_read_bytes"] = tr["read_bytes"]
+            roofline["traffic_write_bytes"] = tr["write_bytes"]
     log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms: {ms * 1e3:.1f} us/step, "
         f"{value:.1f} GB/s effective ({100 * value / HBM_PEAK_GBPS:.1f} % of peak)")
     if roofline:

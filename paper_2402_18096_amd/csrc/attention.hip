@@ -449,8 +449,16 @@ constexpr int unroll_for() { return BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL
 template <int BITS>
 constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PREFETCH_HIGHBIT; }
 
+#ifndef MIKV_WAVES_PER_EU
+#define MIKV_WAVES_PER_EU 1
+#endif
+#ifndef MIKV_CHUNK_KB
+#define MIKV_CHUNK_KB 96
+#endif
+
 template <int HI, int LO, int G, bool SPLITQ>
-__global__ __launch_bounds__(64) void attn_partial_kernel(AttnArgs A) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
+void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G == 8 ? 16 : 32;
   const int h = blockIdx.y, c = blockIdx.x;
   if (c < A.nc_hi)
@@ -462,58 +470,90 @@ __global__ __launch_bounds__(64) void attn_partial_kernel(AttnArgs A) {
 // Softmax over the whole sequence from the chunk records (Section 2.1): a
 // query head's max M is the largest chunk max, its normaliser L the chunk
 // sums rescaled by exp2(m_r - M); the output is the rescaled value sums / L.
-// Every block derives (M, 1/L) of the G query heads of KV head h from the
-// (m, l) pairs, then turns one tile of scores into probabilities (and adds
-// their GQA sum to the importance scores when asked); block 0 also merges
-// the value sums into the output.
-constexpr int kProbTile = 2 * kBlock;  // scores per block and query head
+// Each block of the finalize kernel derives (M, 1/L) of the G query heads of
+// KV head h from the (m, l) pairs, then turns one tile of scores into
+// probabilities (and adds their GQA sum to the importance scores when
+// asked); block 0 also merges the value sums into the output.
+constexpr int kProbTile = 8 * kBlock;  // scores per block and query head
 
-template <int W>
-__device__ inline float max_lanes(float v) {
+// (M, 1/L) of query heads qh0 .. qh0+G-1, computed by every wave on its own
+// (no LDS, no barrier): lane r merges the (m, l) pairs of records r, r+64, ...
+template <int G>
+__device__ inline void head_stats(const AttnArgs &A, int qh0, int nc, float M[G], float inv[G]) {
+  const int lane = threadIdx.x & 63;
+  float m[G], l[G];
 #pragma unroll
-  for (int o = W / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  for (int i = 0; i < G; ++i) {
+    m[i] = kNegInf;
+    l[i] = 0.0f;
+  }
+  for (int r = lane; r < nc; r += 64) {
+    float2 ml[G];
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+      ml[i] = *reinterpret_cast<const float2 *>(A.partials + ((int64_t)(qh0 + i) * nc + r) * kRec);
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      if (ml[i].x > m[i]) {
+        l[i] = fmaf(l[i], __builtin_amdgcn_exp2f(m[i] - ml[i].x), ml[i].y);
+        m[i] = ml[i].x;
+      } else if (ml[i].x != kNegInf) {
+        l[i] = fmaf(ml[i].y, __builtin_amdgcn_exp2f(ml[i].x - m[i]), l[i]);
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    M[i] = wave_max(m[i]);
+    inv[i] = 1.0f / wave_sum(m[i] == kNegInf ? 0.0f : l[i] * __builtin_amdgcn_exp2f(m[i] - M[i]));
+  }
 }
 
 template <int G>
 __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi,
                                                                int tiles_lo) {
-  constexpr int TPH = G <= 4 ? 64 : 32;  // lanes per query head for the statistics
   const int h = blockIdx.y, c = blockIdx.x;
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
-  __shared__ float s_M[G], s_inv[G];
-  {
-    const int i = threadIdx.x / TPH, r0 = threadIdx.x % TPH;
-    float m = kNegInf, l = 0.0f;
-    if (i < G) {
-      const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
-      for (int r = r0; r < nc; r += TPH) {
-        const float2 ml = *reinterpret_cast<const float2 *>(rec + (int64_t)r * kRec);
-        if (ml.x > m) {
-          l = fmaf(l, __builtin_amdgcn_exp2f(m - ml.x), ml.y);
-          m = ml.x;
-        } else if (ml.x != kNegInf) {
-          l = fmaf(ml.y, __builtin_amdgcn_exp2f(ml.x - m), l);
-        }
-      }
-    }
-    const float M = max_lanes<TPH>(m);
-    const float L = sum_lanes<TPH>(m == kNegInf ? 0.0f : l * __builtin_amdgcn_exp2f(m - M));
-    if (i < G && r0 == 0) {
-      s_M[i] = M;
-      s_inv[i] = 1.0f / L;
-    }
+
+  // Probability tile of this block: its scores (and importance scores) are
+  // loaded first, so that their latency overlaps the statistics below.
+  const bool is_hi = c < tiles_hi;
+  const bool has_tile = is_hi || c - tiles_hi < tiles_lo;
+  const int tile = is_hi ? c : c - tiles_hi;
+  const int cap = is_hi ? A.cap_hi : A.cap_lo;
+  const float *scores = is_hi ? A.scores_hi : A.scores_lo;
+  float *probs = is_hi ? A.probs_hi : A.probs_lo;
+  float *acc = is_hi && accumulate ? A.acc : nullptr;
+  constexpr int kPer = kProbTile / kBlock;
+  float sv[kPer][G], a[kPer];
+  int t[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    t[u] = tile * kProbTile + u * kBlock + threadIdx.x;
+    const bool ok = has_tile && t[u] < cap;
+#pragma unroll
+    for (int i = 0; i < G; ++i) sv[u][i] = ok ? scores[(int64_t)(qh0 + i) * cap + t[u]] : 0.0f;
+    a[u] = ok && acc ? acc[(int64_t)h * A.cap_hi + t[u]] : 0.0f;
   }
-  __syncthreads();
+  const int n_pool = has_tile ? (is_hi ? A.n_hi[h] : A.n_lo[h]) : 0;
+
+  float M[G], inv[G];
+  head_stats<G>(A, qh0, nc, M, inv);
 
   if (c == 0) {
-    // Thread -> (record split s, query head i, 4 channels q4).
+    // Output merge.  Thread -> (record split s, query head i, 4 channels q4).
     constexpr int S = 8 / G;
     const int q4 = threadIdx.x % 32, i = (threadIdx.x / 32) % G, s = threadIdx.x / (32 * G);
     const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
-    const float Mi = s_M[i];
+    float Mi = M[0], invi = inv[0];
+#pragma unroll
+    for (int j = 1; j < G; ++j)
+      if (i == j) {
+        Mi = M[j];
+        invi = inv[j];
+      }
     float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 #pragma unroll 4
     for (int r = s; r < nc; r += S) {
@@ -537,38 +577,18 @@ __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int a
         v.z += u.z;
         v.w += u.w;
       }
-      const float inv = s_inv[i];
       reinterpret_cast<float4 *>(A.out + (int64_t)(qh0 + i) * kHeadDim)[q4] =
-          make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv);
+          make_float4(v.x * invi, v.y * invi, v.z * invi, v.w * invi);
     }
   }
 
-  const bool is_hi = c < tiles_hi;
-  if (!is_hi && c - tiles_hi >= tiles_lo) return;
-  const int tile = is_hi ? c : c - tiles_hi;
-  const int n_pool = is_hi ? A.n_hi[h] : A.n_lo[h];
-  const int cap = is_hi ? A.cap_hi : A.cap_lo;
-  const float *scores = is_hi ? A.scores_hi : A.scores_lo;
-  float *probs = is_hi ? A.probs_hi : A.probs_lo;
-  float *acc = is_hi && accumulate ? A.acc : nullptr;
-  constexpr int kPer = kProbTile / kBlock;
-  float sv[kPer][G], a[kPer];
-  int t[kPer];
-#pragma unroll
-  for (int u = 0; u < kPer; ++u) {
-    t[u] = tile * kProbTile + u * kBlock + threadIdx.x;
-    const bool ok = t[u] < n_pool;
-#pragma unroll
-    for (int i = 0; i < G; ++i) sv[u][i] = ok ? scores[(int64_t)(qh0 + i) * cap + t[u]] : 0.0f;
-    a[u] = ok && acc ? acc[(int64_t)h * A.cap_hi + t[u]] : 0.0f;
-  }
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
     if (t[u] >= n_pool) continue;
     float sum = 0.0f;
 #pragma unroll
     for (int i = 0; i < G; ++i) {
-      const float p = __builtin_amdgcn_exp2f(sv[u][i] - s_M[i]) * s_inv[i];
+      const float p = __builtin_amdgcn_exp2f(sv[u][i] - M[i]) * inv[i];
       if (probs) probs[(int64_t)(qh0 + i) * cap + t[u]] = p;
       sum = i == 0 ? p : sum + p;
     }
@@ -605,10 +625,10 @@ Plan make_plan(const mikv_cache *c, int length) {
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int64_t bh = token_bytes(c->hi_bits, c->group), bl = token_bytes(c->lo_bits, c->group);
   const int64_t total = NH * (span_hi * bh + span_lo * bl);
-  // One wave per chunk; ~96 KiB of packed K/V per chunk (many small work
+  // One wave per chunk; up to 96 KiB of packed K/V per chunk (many small work
   // units balance the CUs best), at least 16 KiB so the per-chunk merge
   // stays cheap.  Chunks are whole wave iterations (128 tokens).
-  int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, 96 << 10), 16 << 10);
+  int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, MIKV_CHUNK_KB << 10), 16 << 10);
   p.chunk_hi = std::max(128, round_up(target / bh, 128));
   p.chunk_lo = std::max(128, round_up(target / bl, 128));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
