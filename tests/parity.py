@@ -165,3 +165,89 @@ class Lockstep:
         err_o = float(np.max(np.abs(o_gpu - o_ref)))
         err_p = float(np.max(np.abs(p_gpu - p_ref) / np.maximum(np.abs(p_ref), 1e-30)))
         return err_o, err_p
+
+
+class SampledLockstep:
+    """The benchmark's launch configuration at full size -- every head on the
+    GPU, one mikv_decode_step per token with the importance update fused --
+    checked on a sample of heads that the oracle follows.
+
+    Inside one native step the top-k re-rank runs after attention and moves
+    slots, so the slot -> position map at attention time is rebuilt from the
+    state before the step plus the appended token (slot n_hi, position L-1).
+    """
+
+    def __init__(self, wl, steps, heads):
+        self.wl, self.steps = wl, steps
+        self.heads = sorted(set(int(h) for h in heads))
+        NH, G, T = wl.n_heads, wl.group_size, wl.context
+        dev = "cuda"
+        self.dec = mikv.MikvDecoder(wl, max_len=T + steps, device=dev, fused=True)
+        k, v = workloads.prefill_kv(wl, dev)
+        sc = workloads.initial_scores(wl, dev)
+        qp = workloads.prefill_queries(wl, dev) if wl.balanced else None
+        self.q, self.kn, self.vn = workloads.decode_inputs(wl, steps, dev)
+        sel = torch.tensor(self.heads, device=dev)
+        self.sel = sel
+        self.k_s = np16(k.reshape(NH, T, 128).index_select(0, sel))
+        self.v_s = np16(v.reshape(NH, T, 128).index_select(0, sel))
+        self.sc_s = sc.reshape(NH, T).index_select(0, sel).cpu().numpy()
+        self.qp_s = np16(qp.reshape(NH, G, T, 128).index_select(0, sel)) if qp is not None else None
+        self.dec.prefill(k, v, sc, qp)
+        del k, v, qp
+        self.orc = oracle.OracleCache(len(self.heads), G, self.dec.max_len, wl.hi_bits, wl.lo_bits, wl.group)
+        self.bal = None
+
+    def prefill(self):
+        wl, T = self.wl, self.wl.context
+        if wl.balanced:
+            self.bal = oracle.balancer(self.qp_s, self.k_s)
+            got = self.dec.balance.reshape(wl.n_heads, 128).index_select(0, self.sel).cpu().numpy()
+            np.testing.assert_array_equal(got.view(np.uint32), self.bal.view(np.uint32), err_msg="balancer")
+        kh = oracle.heavy_budget(T, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio)
+        self.orc.prefill(self.k_s, self.v_s, self.sc_s, kh, wl.window, self.bal)
+        torch.cuda.synchronize()
+        compare_state(self.dec.cache, self.orc, heads=self.heads, tag="prefill")
+
+    def _rows(self, t: torch.Tensor, per_head: int):
+        """Rows of the sampled heads of a [B, H*, ...] tensor, as [S, per_head, ...] numpy."""
+        NH = self.wl.n_heads
+        x = t.reshape(NH, per_head, *t.shape[2:]).index_select(0, self.sel)
+        return x.cpu().numpy()
+
+    def step(self, t):
+        wl, G = self.wl, self.wl.group_size
+        c = self.dec.cache
+        S = len(self.heads)
+        n_hi0 = c.n_hi.index_select(0, self.sel).cpu().numpy()
+        n_lo0 = c.n_lo.index_select(0, self.sel).cpu().numpy()
+        hi_pos0 = c.hi_pos.index_select(0, self.sel).cpu().numpy()
+        lo_pos0 = c.lo_pos.index_select(0, self.sel).cpu().numpy()
+        self.dec.step_native(self.q[t], self.kn[t], self.vn[t])
+        torch.cuda.synchronize()
+        L = self.dec.length
+        assert int(c.status.item()) == 0, f"step {t}: device status {int(c.status.item())}"
+        # slot -> position map as it was during attention
+        n_hi_att = n_hi0 + 1
+        hi_pos_att = hi_pos0.copy()
+        for i in range(S):
+            hi_pos_att[i, n_hi0[i]] = L - 1
+        ph = self._rows(self.dec.probs_hi, G)
+        pl = self._rows(self.dec.probs_lo, G)
+        p_gpu = np.full((S, G, L), np.nan, np.float32)
+        for i in range(S):
+            p_gpu[i][:, hi_pos_att[i, :n_hi_att[i]]] = ph[i, :, :n_hi_att[i]]
+            p_gpu[i][:, lo_pos0[i, :n_lo0[i]]] = pl[i, :, :n_lo0[i]]
+        o_gpu = self._rows(self.dec.out, G)
+        kn = np16(self.kn[t].reshape(wl.n_heads, 128).index_select(0, self.sel))
+        vn = np16(self.vn[t].reshape(wl.n_heads, 128).index_select(0, self.sel))
+        self.orc.append(kn, vn, self.bal)
+        q = np16(self.q[t].reshape(wl.n_heads, G, 128).index_select(0, self.sel))
+        o_ref, p_ref = self.orc.attend(q, SCALE, self.bal)
+        np.testing.assert_allclose(o_gpu, o_ref, atol=O_ATOL, rtol=O_RTOL, err_msg=f"step {t}: attention output")
+        assert not np.isnan(p_gpu).any(), f"step {t}: a position got no probability"
+        np.testing.assert_allclose(p_gpu, p_ref, atol=P_ATOL, rtol=P_RTOL, err_msg=f"step {t}: probabilities")
+        self.orc.accumulate(p_gpu)
+        kh = oracle.heavy_budget(L, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio)
+        self.orc.select(kh, wl.window)
+        compare_state(c, self.orc, heads=self.heads, tag=f"step {t}")

@@ -12,7 +12,7 @@ import torch
 
 import oracle
 from paper_2402_18096_amd import mikv, workloads
-from tests.parity import Lockstep, compare_state, np16
+from tests.parity import Lockstep, SampledLockstep, compare_state, np16
 
 pytestmark = pytest.mark.gpu
 
@@ -133,6 +133,25 @@ def test_lockstep_decode(name, fused):
     run.prefill()
     for t in range(steps):
         run.step(t)
+
+
+@pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
+def test_full_size_sampled_heads(name):
+    """Every workload at its full size, in the benchmark's launch configuration
+    (one native call per step, importance fused, probabilities of both pools
+    emitted), with the oracle following the first, a middle and the last
+    head: bit-exact state, attention and probabilities within tolerance."""
+    _dev()
+    wl = workloads.WORKLOADS[name]
+    NH = wl.n_heads
+    steps = min(wl.steps, 3)
+    print(f"[full-size] {name}: {NH} heads, context {wl.context}, {steps} steps", flush=True)
+    run = SampledLockstep(wl, steps, heads=[0, NH // 2 + 1 if NH > 2 else 0, NH - 1])
+    run.prefill()
+    for t in range(steps):
+        run.step(t)
+    del run
+    torch.cuda.empty_cache()
 
 
 def test_lockstep_gqa8():
