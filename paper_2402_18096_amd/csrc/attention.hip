@@ -49,6 +49,7 @@ constexpr int kRec = kRecO + kHeadDim;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLazy = 8.0f;       // raise the running max only past this (log2 units)
+constexpr int kMaxChunk = 1024;     // tokens per chunk at most (the chunk's scores are held in LDS)
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
@@ -202,7 +203,7 @@ __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, r
 }
 
 template <int BITS, int G, int CPL, bool SPLITQ, int UNROLL, int PREFETCH>
-__device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, bool is_hi) {
+__device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, bool is_hi, float *s_lds) {
   using F = Fmt<BITS>;
   constexpr int LPT = kHeadDim / CPL, TPW = 64 / LPT, NP = CPL / 2;
   constexpr bool Q = F::kQuant;
@@ -213,7 +214,11 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 
   const int cap = is_hi ? A.cap_hi : A.cap_lo;
   const int chunk_len = is_hi ? A.chunk_hi : A.chunk_lo;
-  const int n_pool = is_hi ? A.n_hi[h] : A.n_lo[h];
+  // The pool count comes through a vector load; make it provably
+  // wave-uniform, so the buffer descriptors built from it live in scalar
+  // registers (a value the compiler thinks divergent would wrap every load in
+  // a per-lane loop).
+  const int n_pool = __builtin_amdgcn_readfirstlane(is_hi ? A.n_hi[h] : A.n_lo[h]);
   const int start = chunk * chunk_len;
   const int end = min(start + chunk_len, n_pool);
   constexpr int64_t kRow = BITS == 16 ? kHeadDim * 2 : kHeadDim * BITS / 8;
@@ -228,30 +233,6 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   // Query (Eq. 4: q / balance), as fp16 pairs matching the format's pairing,
   // each pair pre-scaled by 2^-cls; with SPLITQ a second fp16 pair carries
   // the rounding remainder.  qsum = sum of the lane's query channels (fp32).
-  half2_t qh[G][NP], ql[G][SPLITQ ? NP : 1];
-  float qsum[G];
-#pragma unroll
-  for (int i = 0; i < G; ++i) {
-    const uint16_t *qrow = A.q + (int64_t)(qh0 + i) * kHeadDim + part * CPL;
-    const float *brow = A.balance ? A.balance + (int64_t)h * kHeadDim + part * CPL : nullptr;
-    auto qhat = [&](int c) {
-      float v = f16_to_f32(qrow[c]);
-      return brow ? v / brow[c] : v;
-    };
-    float s = 0.0f;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) s += qhat(c);
-    qsum[i] = s;
-#pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      const float sc = __builtin_ldexpf(1.0f, -F::cls(p));
-      const float a = qhat(F::lo(p)) * sc, bb = qhat(F::hi(p)) * sc;
-      const _Float16 ah = (_Float16)a, bh = (_Float16)bb;
-      qh[i][p] = half2_t{ah, bh};
-      if constexpr (SPLITQ) ql[i][p] = half2_t{(_Float16)(a - (float)ah), (_Float16)(bb - (float)bh)};
-    }
-  }
-
   float m2[G], l[G], bsum[G], o[G][CPL];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
@@ -263,6 +244,9 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   }
 
   constexpr int kPerIter = kWaves * TPW * UNROLL;
+  // chunks are whole multiples of 128 tokens, at most kMaxChunk: an
+  // iteration never runs past the LDS score buffer
+  static_assert(128 % kPerIter == 0 && kMaxChunk % 128 == 0, "iteration must divide 128 tokens");
   constexpr int kSeg = Rows<BITS, CPL>::KW * 4;  // bytes of one lane's row segment
   const int n_iter = end > start ? (end - start + kPerIter - 1) / kPerIter : 0;
   const int first = start + wave * TPW * UNROLL + tsub;  // this lane's token in iteration 0, u = 0
@@ -287,6 +271,75 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
                                opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u);
   };
 
+  // The first iterations' rows do not depend on the query: issue them first.
+  Rows<BITS, CPL> cur[UNROLL], n1[PREFETCH >= 1 ? UNROLL : 1], n2[PREFETCH >= 2 ? UNROLL : 1];
+  if (n_iter > 0) load_it(cur, 0);
+  if constexpr (PREFETCH >= 1) {
+    if (n_iter > 1) load_it(n1, 1);
+  }
+  if constexpr (PREFETCH >= 2) {
+    if (n_iter > 2) load_it(n2, 2);
+  }
+
+  // Every query (and balancer) word this lane needs is loaded with 16-byte
+  // loads issued together, before any of them is used: the chunk's K/V
+  // stream starts one memory round trip after the wave does.
+  half2_t qh[G][NP], ql[G][SPLITQ ? NP : 1];
+  float qsum[G];
+  uint4 qraw[G][CPL / 8];
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    const uint4 *q4 = reinterpret_cast<const uint4 *>(A.q + (int64_t)(qh0 + i) * kHeadDim + part * CPL);
+#pragma unroll
+    for (int j = 0; j < CPL / 8; ++j) qraw[i][j] = q4[j];
+  }
+  float bal[SPLITQ ? CPL : 1];
+  if constexpr (SPLITQ) {
+    const float4 *b4 = reinterpret_cast<const float4 *>(A.balance + (int64_t)h * kHeadDim + part * CPL);
+#pragma unroll
+    for (int j = 0; j < CPL / 4; ++j) {
+      const float4 v = b4[j];
+      bal[4 * j] = v.x;
+      bal[4 * j + 1] = v.y;
+      bal[4 * j + 2] = v.z;
+      bal[4 * j + 3] = v.w;
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    float qf[CPL];
+#pragma unroll
+    for (int j = 0; j < CPL / 8; ++j) {
+      const uint32_t w[4] = {qraw[i][j].x, qraw[i][j].y, qraw[i][j].z, qraw[i][j].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        qf[8 * j + 2 * k] = f16_to_f32((uint16_t)(w[k] & 0xffffu));
+        qf[8 * j + 2 * k + 1] = f16_to_f32((uint16_t)(w[k] >> 16));
+      }
+    }
+    if constexpr (SPLITQ) {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) qf[c] = qf[c] / bal[c];
+    }
+    auto qhat = [&](int c) { return qf[c]; };
+    float s = 0.0f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) s += qhat(c);
+    qsum[i] = s;
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const float sc = __builtin_ldexpf(1.0f, -F::cls(p));
+      const float a = qhat(F::lo(p)) * sc, bb = qhat(F::hi(p)) * sc;
+      const _Float16 ah = (_Float16)a, bh = (_Float16)bb;
+      qh[i][p] = half2_t{ah, bh};
+      if constexpr (SPLITQ) ql[i][p] = half2_t{(_Float16)(a - (float)ah), (_Float16)(bb - (float)bh)};
+    }
+  }
+
+  // The chunk's scores stay in LDS (written by the lanes that hold them)
+  // and go out in one burst after the loop: no global store is issued
+  // between the loads of the stream (stores and loads share one completion
+  // counter, so stores in the loop delay every later load wait).
   float *score_row[G];
 #pragma unroll
   for (int i = 0; i < G; ++i) score_row[i] = scores ? scores + (int64_t)(qh0 + i) * cap : nullptr;
@@ -319,7 +372,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
         s = token_sum<LPT>(s) * s2scale;
         s = valid[u] ? s : kNegInf;
         s2[u][i] = s;
-        if (scores && valid[u] && part == 0) score_row[i][t] = s;
+        if (scores && part == 0) s_lds[i * kMaxChunk + it * kPerIter + u * TPW + tsub] = s;
         raise = raise || (s > m2[i] + kLazy);
       }
     }
@@ -367,34 +420,36 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 
   // Software pipeline: the rows of the next PREFETCH iterations are loaded
   // while the current one is computed.
-  Rows<BITS, CPL> cur[UNROLL];
   if constexpr (PREFETCH == 0) {
     for (int it = 0; it < n_iter; ++it) {
-      load_it(cur, it);
+      if (it > 0) load_it(cur, it);
       proc(cur, it);
     }
   } else if constexpr (PREFETCH == 1) {
-    Rows<BITS, CPL> n1[UNROLL];
-    if (n_iter > 0) load_it(cur, 0);
     for (int it = 0; it < n_iter; ++it) {
-      if (it + 1 < n_iter) load_it(n1, it + 1);
       proc(cur, it);
 #pragma unroll
       for (int u = 0; u < UNROLL; ++u) cur[u] = n1[u];
+      if (it + 2 < n_iter) load_it(n1, it + 2);
     }
   } else {
-    Rows<BITS, CPL> n1[UNROLL], n2[UNROLL];
-    if (n_iter > 0) load_it(cur, 0);
-    if (n_iter > 1) load_it(n1, 1);
     for (int it = 0; it < n_iter; ++it) {
-      if (it + 2 < n_iter) load_it(n2, it + 2);
       proc(cur, it);
 #pragma unroll
       for (int u = 0; u < UNROLL; ++u) {
         cur[u] = n1[u];
         n1[u] = n2[u];
       }
+      if (it + 3 < n_iter) load_it(n2, it + 3);
     }
+  }
+  if (scores) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+      for (int j = lane; j < end - start; j += 64) score_row[i][start + j] = s_lds[i * kMaxChunk + j];
   }
 
   // Undo the code scaling, add the beta part, merge the lanes of equal
@@ -461,10 +516,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_P
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G == 8 ? 16 : 32;
   const int h = blockIdx.y, c = blockIdx.x;
+  __shared__ float s_lds[G * kMaxChunk];  // the chunk's scores, [G][kMaxChunk]
   if (c < A.nc_hi)
-    attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true);
+    attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
   else
-    attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false);
+    attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
 }
 
 // Softmax over the whole sequence from the chunk records (Section 2.1): a
@@ -629,8 +685,8 @@ Plan make_plan(const mikv_cache *c, int length) {
   // units balance the CUs best), at least 16 KiB so the per-chunk merge
   // stays cheap.  Chunks are whole wave iterations (128 tokens).
   int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, MIKV_CHUNK_KB << 10), 16 << 10);
-  p.chunk_hi = std::max(128, round_up(target / bh, 128));
-  p.chunk_lo = std::max(128, round_up(target / bl, 128));
+  p.chunk_hi = std::min(kMaxChunk, std::max(128, round_up(target / bh, 128)));
+  p.chunk_lo = std::min(kMaxChunk, std::max(128, round_up(target / bl, 128)));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
   p.nc_lo = std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
   return p;
@@ -699,11 +755,13 @@ void launch_partial_g(const AttnArgs &A, int G, dim3 grid, hipStream_t st) {
     launch_partial_q<HI, LO, false>(A, G, grid, st);
 }
 
-int check_attention_args(const mikv_cache *c, int32_t length, const uint16_t *q, float *out, void *ws,
-                         size_t ws_bytes, const char *who) {
+int check_attention_args(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float *out,
+                         void *ws, size_t ws_bytes, const char *who) {
   int rc = validate_cache(c);
   if (rc) return rc;
   if (!q || !out) return set_error(MIKV_ERR_INVALID_ARG, "%s: q/out is NULL", who);
+  if (((uintptr_t)q | (uintptr_t)balance) % 16 != 0)
+    return set_error(MIKV_ERR_INVALID_ARG, "%s: q and balance must be 16-byte aligned", who);
   if (length < 1) return set_error(MIKV_ERR_INVALID_ARG, "%s: length must be >= 1", who);
   if (length > c->max_len) return set_error(MIKV_ERR_CAPACITY, "%s: length %d > max_len %d", who, length, c->max_len);
   Plan p = make_plan(c, length);
@@ -727,7 +785,7 @@ extern "C" int mikv_decode_attention_partial(const mikv_cache *c, int32_t length
                                              const float *balance, float scale, float *out, float *probs_hi,
                                              float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
                                              void *stream) {
-  int rc = check_attention_args(c, length, q, out, ws, ws_bytes, "mikv_decode_attention_partial");
+  int rc = check_attention_args(c, length, q, balance, out, ws, ws_bytes, "mikv_decode_attention_partial");
   if (rc) return rc;
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, flags, ws);
@@ -749,7 +807,7 @@ extern "C" int mikv_decode_attention_finalize(const mikv_cache *c, int32_t lengt
                                               const float *balance, float scale, float *out, float *probs_hi,
                                               float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
                                               void *stream) {
-  int rc = check_attention_args(c, length, q, out, ws, ws_bytes, "mikv_decode_attention_finalize");
+  int rc = check_attention_args(c, length, q, balance, out, ws, ws_bytes, "mikv_decode_attention_finalize");
   if (rc) return rc;
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, flags, ws);
