@@ -62,6 +62,15 @@ __host__ __device__ inline uint16_t f32_to_f16_rne(float f) {
   return (uint16_t)(sign | r);
 }
 
+// Two fp32 values to an fp16 pair (low half first) with the hardware
+// conversion: IEEE round to nearest even, fp16 subnormals kept (the default
+// floating-point mode these kernels run in).  Used for stored fp16 rows; the
+// per-group scale and zero use f32_to_f16_rne above.
+__device__ inline uint32_t pack_f16x2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+}
+
 __device__ inline float f16_to_f32(uint16_t h) {
   return (float)__builtin_bit_cast(_Float16, h);
 }

@@ -243,7 +243,7 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
           uint32_t w[16];
 #pragma unroll
           for (int c = 0; c < 16; ++c)
-            w[c] = (uint32_t)f32_to_f16_rne(x[2 * c]) | ((uint32_t)f32_to_f16_rne(x[2 * c + 1]) << 16);
+            w[c] = pack_f16x2(x[2 * c], x[2 * c + 1]);
           uint4 *d4 = reinterpret_cast<uint4 *>(dst);
 #pragma unroll
           for (int i = 0; i < 4; ++i) d4[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
@@ -292,7 +292,7 @@ __global__ __launch_bounds__(64) void append_one_kernel(Pools P, const uint16_t 
       uint32_t w[16];
 #pragma unroll
       for (int c = 0; c < 16; ++c)
-        w[c] = (uint32_t)f32_to_f16_rne(x[2 * c]) | ((uint32_t)f32_to_f16_rne(x[2 * c + 1]) << 16);
+        w[c] = pack_f16x2(x[2 * c], x[2 * c + 1]);
       uint4 *d4 = reinterpret_cast<uint4 *>((is_v ? P.hi_v : P.hi_k) + (slot * kHeadDim + lane4 * 32) * 2);
 #pragma unroll
       for (int i = 0; i < 4; ++i) d4[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);

@@ -213,27 +213,55 @@ __device__ inline void demote_row(const SelArgs &A, int h, int slot, int64_t lsl
   }
 }
 
-// Move importance-pool slot src into slot dst (rows, position, score and,
-// for INT8 rows, the scale/zero words); the whole block takes part.
+// One importance-pool slot's data (rows, position, score and, for INT8
+// rows, the scale/zero words), spread over the block: threads below
+// 2 * row/16 hold a 16-byte piece of the K or V row, threads 64.. a scale
+// word, thread 0 the position and score.  Loaded early, stored late.
 template <int HI_BITS>
-__device__ inline void move_slot(const SelArgs &A, int h, int src, int dst, int p, float a) {
-  const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
-  constexpr int chunks = (HI_BITS == 16 ? 2 * kHeadDim : kHeadDim) / 16;
+struct SlotData {
+  uint4 piece;
+  uint32_t par;
+  int pos;
+  float acc;
+};
+
+template <int HI_BITS>
+__device__ inline SlotData<HI_BITS> load_slot(const SelArgs &A, int h, int src) {
+  constexpr int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  constexpr int chunks = hrow / 16;
+  const int ng = kHeadDim / A.group;
+  SlotData<HI_BITS> d{};
+  if (threadIdx.x < 2 * chunks) {
+    const uint8_t *base = (threadIdx.x < chunks ? A.hi_k : A.hi_v) + (int64_t)h * A.cap_hi * hrow;
+    d.piece = reinterpret_cast<const uint4 *>(base + (int64_t)src * hrow)[threadIdx.x % chunks];
+  }
+  if (HI_BITS == 8 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
+    const uint32_t *pp = threadIdx.x - 64 < ng ? A.hi_kp : A.hi_vp;
+    d.par = pp[((int64_t)h * A.cap_hi + src) * ng + (threadIdx.x - 64) % ng];
+  }
+  if (threadIdx.x == 0) {
+    d.pos = A.hi_pos[(int64_t)h * A.cap_hi + src];
+    d.acc = A.hi_acc[(int64_t)h * A.cap_hi + src];
+  }
+  return d;
+}
+
+template <int HI_BITS>
+__device__ inline void store_slot(const SelArgs &A, int h, int dst, const SlotData<HI_BITS> &d) {
+  constexpr int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  constexpr int chunks = hrow / 16;
   const int ng = kHeadDim / A.group;
   if (threadIdx.x < 2 * chunks) {
     uint8_t *base = (threadIdx.x < chunks ? A.hi_k : A.hi_v) + (int64_t)h * A.cap_hi * hrow;
-    const int ck = threadIdx.x % chunks;
-    reinterpret_cast<uint4 *>(base + (int64_t)dst * hrow)[ck] =
-        reinterpret_cast<const uint4 *>(base + (int64_t)src * hrow)[ck];
-  }
-  if (threadIdx.x == 0) {
-    A.hi_pos[(int64_t)h * A.cap_hi + dst] = p;
-    A.hi_acc[(int64_t)h * A.cap_hi + dst] = a;
+    reinterpret_cast<uint4 *>(base + (int64_t)dst * hrow)[threadIdx.x % chunks] = d.piece;
   }
   if (HI_BITS == 8 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
-    const int g = (threadIdx.x - 64) % ng;
     uint32_t *pp = threadIdx.x - 64 < ng ? A.hi_kp : A.hi_vp;
-    pp[((int64_t)h * A.cap_hi + dst) * ng + g] = pp[((int64_t)h * A.cap_hi + src) * ng + g];
+    pp[((int64_t)h * A.cap_hi + dst) * ng + (threadIdx.x - 64) % ng] = d.par;
+  }
+  if (threadIdx.x == 0) {
+    A.hi_pos[(int64_t)h * A.cap_hi + dst] = d.pos;
+    A.hi_acc[(int64_t)h * A.cap_hi + dst] = d.acc;
   }
 }
 
@@ -245,8 +273,8 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
   __shared__ int s_tmp_i[kSel / 64];
   __shared__ uint64_t s_tmp_u[kSel / 64];
   __shared__ int s_arg[3];
-  const int n = A.n_hi[h];
-  const int n_lo0 = A.n_lo[h];
+  const int n = __builtin_amdgcn_readfirstlane(A.n_hi[h]);
+  const int n_lo0 = __builtin_amdgcn_readfirstlane(A.n_lo[h]);
   const int thr = A.length - A.window;  // positions >= thr are in the window
   const int32_t *pos = A.hi_pos + (int64_t)h * A.cap_hi;
   const float *acc = A.hi_acc + (int64_t)h * A.cap_hi;
@@ -254,21 +282,22 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
   auto key = [&](int i) { return rank_key(acc[i], pos[i]); };
 
   // One pass over the pool, kSel * kSelItems slots per round trip: count
-  // the eligible slots and keep the least important one.
+  // the eligible slots and keep the least important one.  The loads run to
+  // the capacity, so they need not wait for the pool count.
   int cnt = 0, arg = -1;
   uint64_t mn = ~0ull;
-  for (int base = 0; base < n; base += kSel * kSelItems) {
+  for (int base = 0; base < A.cap_hi; base += kSel * kSelItems) {
     int pv[kSelItems];
     float av[kSelItems];
 #pragma unroll
     for (int u = 0; u < kSelItems; ++u) {
       const int i = base + u * kSel + threadIdx.x;
-      pv[u] = i < n ? pos[i] : thr;
-      av[u] = i < n ? acc[i] : 0.0f;
+      pv[u] = i < A.cap_hi ? pos[i] : thr;
+      av[u] = i < A.cap_hi ? acc[i] : 0.0f;
     }
 #pragma unroll
     for (int u = 0; u < kSelItems; ++u) {
-      if (pv[u] < thr) {
+      if (base + u * kSel + (int)threadIdx.x < n && pv[u] < thr) {
         ++cnt;
         const uint64_t k = rank_key(av[u], pv[u]);
         if (k < mn) {
@@ -278,6 +307,9 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
       }
     }
   }
+  // The last slot fills the hole of a demoted token: fetch it now, its
+  // latency then hides behind the reductions.
+  const SlotData<HI_BITS> last = n > 0 ? load_slot<HI_BITS>(A, h, n - 1) : SlotData<HI_BITS>{};
   const int n_elig = block_sum_int(cnt, s_tmp_i);
   const int n_dem = n_elig - A.k_heavy;
   if (n_dem <= 0) return;
@@ -290,19 +322,13 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
     // Steady state of decoding: the least important eligible token leaves;
     // the last slot fills its hole.
     const uint64_t cut = block_min_u64(mn, s_tmp_u);
-    if (arg >= 0 && mn == cut) {
-      s_arg[0] = arg;
-      s_arg[1] = pos[arg];
-    }
-    if (threadIdx.x == 0) {
-      s_arg[2] = pos[n - 1];
-      s_tmp_u[0] = __float_as_uint(acc[n - 1]);
-    }
+    if (arg >= 0 && mn == cut) s_arg[0] = arg;
     __syncthreads();
     const int slot = s_arg[0];
-    demote_row<HI_BITS, LO_BITS>(A, h, slot, (int64_t)h * A.cap_lo + n_lo0, s_arg[1]);
+    // the key's low word is the position
+    demote_row<HI_BITS, LO_BITS>(A, h, slot, (int64_t)h * A.cap_lo + n_lo0, (int)(uint32_t)cut);
     __syncthreads();
-    if (slot != n - 1) move_slot<HI_BITS>(A, h, n - 1, slot, s_arg[2], __uint_as_float((uint32_t)s_tmp_u[0]));
+    if (slot != n - 1) store_slot<HI_BITS>(A, h, slot, last);
     if (threadIdx.x == 0) {
       A.n_hi[h] = n - 1;
       A.n_lo[h] = n_lo0 + 1;

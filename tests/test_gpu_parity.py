@@ -221,3 +221,41 @@ def test_native_step_matches_call_sequence(name, fused):
         torch.cuda.synchronize()
         compare_state(other.cache, run.orc, tag=f"native step {t}")
         np.testing.assert_array_equal(other.out.cpu().numpy(), run.dec.out.cpu().numpy())
+
+
+def test_fp16_pool_rounding_edge_cases():
+    """fp16 importance-pool rows are f16(f32(k) * b) with round to nearest
+    even (Eq. 3): balance factors chosen so that every product is an exact
+    tie (1 + 2^-11), lands in the fp16 subnormal range (2^-16), overflows
+    (2^12) or rounds generically; both the many-token placement and the
+    one-token append store bit-for-bit what the oracle stores."""
+    dev = _dev()
+    B, H, n, n1 = 1, 2, 40, 8
+    c = mikv.MikvCache(B, H, H, 32, 16, 2, cap_hi=64, cap_lo=64, max_len=64, device=dev)
+    rng = np.random.default_rng(5)
+    k = (rng.standard_normal((B, H, n + n1, 128)) * 8).astype(np.float16)
+    # m * 2^-24 (m < 2048: fp16 subnormals and the smallest normals) halved:
+    # an exact tie whenever m is odd, rounding to the even neighbour
+    m = rng.integers(1, 2048, (B, H, n + n1, 16)) * rng.choice([-1, 1], (B, H, n + n1, 16))
+    k[..., :16] = (m * 2.0 ** -24).astype(np.float16)
+    k[..., 16:24] = rng.choice([-1.0, 1.0], (B, H, n + n1, 8)).astype(np.float16)  # 1 + 2^-11: a tie
+    b = np.empty((B, H, 128), np.float32)
+    b[..., :16] = np.float32(0.5)
+    b[..., 16:32] = np.float32(1 + 2.0 ** -11)
+    b[..., 32:64] = np.float32(2.0 ** -16)
+    b[..., 64:96] = rng.uniform(0.3, 3.7, (B, H, 32)).astype(np.float32)
+    b[..., 96:] = np.float32(2.0 ** 12)
+    kt = torch.from_numpy(k.view(np.int16)).view(torch.float16).to(dev)
+    bt = torch.from_numpy(b).to(dev)
+    mikv.mikv_quantize_kv(c, kt[:, :, :n].contiguous(), kt[:, :, :n].contiguous(), 0, balance=bt)
+    for j in range(n1):
+        kj = kt[:, :, n + j:n + j + 1].contiguous()
+        mikv.mikv_quantize_kv(c, kj, kj.clone(), n + j, balance=bt)
+    torch.cuda.synchronize()
+    assert int(c.status.item()) == 0
+    got = c.hi_k.cpu().numpy().view(np.uint16)[:, : n + n1]
+    want = oracle.f16_bits(oracle.balance_keys(k.reshape(H, n + n1, 128), b.reshape(H, 1, 128)))
+    assert np.isinf(want.view(np.float16)).any() and ((want & 0x7c00) == 0).any()
+    exact = k.reshape(H, n + n1, 128)[..., :16].astype(np.float64) * 0.5
+    assert (exact != want[..., :16].view(np.float16).astype(np.float64)).any()   # ties were rounded
+    np.testing.assert_array_equal(got, want)
