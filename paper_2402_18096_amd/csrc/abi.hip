@@ -45,6 +45,10 @@ int validate_cache(const mikv_cache *c) {
     return set_error(MIKV_ERR_UNSUPPORTED, "lo_bits must be 2, 4 or 8 (got %d)", c->lo_bits);
   if (c->cap_hi < 1 || c->cap_lo < 1 || c->max_len < 1)
     return set_error(MIKV_ERR_INVALID_ARG, "cap_hi, cap_lo and max_len must be >= 1");
+  if (int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) && c->cap_lo % 32 != 0)
+    return set_error(MIKV_ERR_INVALID_ARG,
+                     "cap_lo must be a multiple of 32 for a 2-bit retained pool shared by query heads (got %d)",
+                     c->cap_lo);
   if (!c->hi_k || !c->hi_v || !c->hi_pos || !c->hi_acc || !c->n_hi || !c->lo_k || !c->lo_v ||
       !c->lo_kp || !c->lo_vp || !c->lo_pos || !c->n_lo || !c->status)
     return set_error(MIKV_ERR_INVALID_ARG, "a required cache pointer is NULL");

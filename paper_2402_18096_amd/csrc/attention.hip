@@ -485,6 +485,420 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   }
 }
 
+// ---------------------------------------------------------------------------
+// The 2-bit retained pool on the matrix cores (16x16x32 fp16 MFMA).
+//
+// Lane l = 16 a + n.  Scores of a 16-token tile: B holds the tile's key
+// codes as exact fp16 subnormals (code * 2^(2k-24), k the code's position
+// class); lane (n, a) holds the 32 codes of channels [32a, 32a + 32) of
+// token n, so the token-major key rows are read as they are stored.  A
+// holds the query: row 4 s + gamma carries q_hat (times 2^-2k) of query
+// slot s on the channels of quantization group gamma and 0 elsewhere, so
+// lane (n, a) receives, for query slot a, one partial dot product per group
+// and applies token n's per-group scale and zero (folded Eq. 1).
+//
+// Value sums: the pool's value codes are stored in 32-slot tiles,
+// quad-major (int2_v_byte).  For n-block nb (channels 16nb..16nb+15) lane
+// (n, g) reads the 8 bytes of quad 4nb + n/4 for slots 8g..8g+7 and keeps
+// field n%4: B = codes (tokens x channels, column scale 2^(2(n%4)-24), undone
+// on the output); A = the softmax weights e * alpha of the column's group,
+// split in an fp16 high and low part (rows 2i and 2i+1 for query i) and
+// staged through LDS into the operand layout.
+// ---------------------------------------------------------------------------
+typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
+
+__device__ inline h8_t pack_h8(uint32_t x, uint32_t y, uint32_t z, uint32_t w) {
+  const u4_t u = {x, y, z, w};
+  return __builtin_bit_cast(h8_t, u);
+}
+
+__device__ inline f4_t mfma32(h8_t a, h8_t b, f4_t c) { return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0); }
+
+// Reductions over the 16 lanes of each row (lane group); result in all 16.
+__device__ inline float row_max16(float v) {
+  v = fmaxf(v, dpp_mov<0xB1>(v));
+  v = fmaxf(v, dpp_mov<0x4E>(v));
+  v = fmaxf(v, dpp_mov<0x141>(v));
+  return fmaxf(v, dpp_mov<0x140>(v));
+}
+__device__ inline float row_sum16(float v) {
+  v += dpp_mov<0xB1>(v);
+  v += dpp_mov<0x4E>(v);
+  v += dpp_mov<0x141>(v);
+  return v + dpp_mov<0x140>(v);
+}
+
+constexpr int kItTok = 64;                     // tokens per iteration: four key tiles, two value tiles
+// Operand element -> slot inside a lane group's 8 (and back): bits 0 and 1
+// swapped, the order the masked code pairs come out in.
+__host__ __device__ constexpr int tau8(int e) { return (e & 4) | ((e & 1) << 1) | ((e >> 1) & 1); }
+
+// LDS weight staging: [group][value tile][row 0..15][lane group][element]
+// halves; rows past 2G stay zero, so every lane reads its operand.
+__device__ inline int w_index(int gamma, int vt, int row, int g, int e) {
+  return (((gamma * 2 + vt) * 16 + row) * 4 + g) * 8 + e;
+}
+constexpr int kWLds = 4 * 2 * 16 * 4 * 8;  // halves (8 KiB)
+
+template <int G, bool SPLITQ, int NG>
+__device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chunk, float *s_lds, _Float16 *w_lds) {
+  constexpr int QS = G < 4 ? G : 4;    // distinct query slots in one row block
+  constexpr int NSET = G > 4 ? 2 : 1;  // query sets (G = 8: queries 0-3 and 4-7)
+  constexpr int R = 4 / QS;            // lane groups holding the same query slot
+  constexpr int NGL = (NG + R - 1) / R;  // value groups each lane weights
+  constexpr int NP = SPLITQ ? 2 : 1;   // fp16 parts of the query
+  constexpr int GROUP = kHeadDim / NG;
+  const int lane = threadIdx.x & 63, n = lane & 15, a = lane >> 4;
+  const int qs = a % QS, rho = a / QS;
+  const int b = h / A.kv_heads, kvh = h % A.kv_heads;
+  const int qh0 = b * A.q_heads + kvh * G;
+  const int cap = A.cap_lo;
+  const int n_pool = __builtin_amdgcn_readfirstlane(A.n_lo[h]);
+  const int start = chunk * A.chunk_lo;
+  const int end = min(start + A.chunk_lo, n_pool);
+  const int n_iter = end > start ? (end - start + kItTok - 1) / kItTok : 0;
+  float *scores = A.scores_lo;
+  const float s2scale = A.scale * kLog2e;
+
+  const rsrc_t rk = make_rsrc(A.lo_k + (int64_t)h * cap * 32, (uint32_t)n_pool * 32u);
+  const rsrc_t rv = make_rsrc(A.lo_v + (int64_t)h * cap * 32, (uint32_t)((n_pool + 31) / 32) * 1024u);
+  const rsrc_t rkp = make_rsrc(A.lo_kp + (int64_t)h * cap * NG, (uint32_t)n_pool * NG * 4u);
+  const rsrc_t rvp = make_rsrc(A.lo_vp + (int64_t)h * cap * NG, (uint32_t)n_pool * NG * 4u);
+
+  // One iteration's loads: key codes and parameter rows of the four key
+  // tiles (the lane's value groups only), value codes of the two tiles.
+  struct Ld {
+    uint32_t kc[4][2];
+    uint32_t kp[4][NG];
+    uint32_t vp[4][NGL];
+    uint32_t vc[2][8][2];
+  };
+  auto load = [&](Ld &d, int it) {
+    const uint32_t t0 = (uint32_t)(start + it * kItTok);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t slot = t0 + 16 * q + n;
+      auto kc = __builtin_amdgcn_raw_buffer_load_b64(rk, slot * 32u + 8u * a, 0, 0);
+      d.kc[q][0] = kc[0];
+      d.kc[q][1] = kc[1];
+      if constexpr (NG == 4) {
+        auto kp = __builtin_amdgcn_raw_buffer_load_b128(rkp, slot * 16u, 0, 0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) d.kp[q][j] = kp[j];
+      } else if constexpr (NG == 2) {
+        auto kp = __builtin_amdgcn_raw_buffer_load_b64(rkp, slot * 8u, 0, 0);
+        d.kp[q][0] = kp[0];
+        d.kp[q][1] = kp[1];
+      } else {
+        d.kp[q][0] = __builtin_amdgcn_raw_buffer_load_b32(rkp, slot * 4u, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < NGL; ++j)
+        d.vp[q][j] = __builtin_amdgcn_raw_buffer_load_b32(rvp, (slot * NG + (uint32_t)((rho + R * j) % NG)) * 4u, 0, 0);
+    }
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt) {
+      const uint32_t tile = (t0 >> 5) + vt;
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        auto vc = __builtin_amdgcn_raw_buffer_load_b64(rv, tile * 1024u + (uint32_t)(4 * nb + n / 4) * 32u + 8u * a, 0, 0);
+        d.vc[vt][nb][0] = vc[0];
+        d.vc[vt][nb][1] = vc[1];
+      }
+    }
+  };
+  Ld cur;
+  if (n_iter > 0) load(cur, 0);
+
+  // zero the weight rows (rows past 2G are never written)
+  {
+    uint4 *w4 = reinterpret_cast<uint4 *>(w_lds);
+#pragma unroll
+    for (int j = 0; j < kWLds / 8 / 64; ++j) w4[j * 64 + lane] = make_uint4(0u, 0u, 0u, 0u);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+
+  // Query operands.  As an A row, lane l is row m = n: query slot m/4 (mod
+  // QS) of set st, group m%4, over K block a (channels [32a, 32a + 32)).
+  h8_t AK[NSET][NP][4];
+  float qpart[NSET];
+#pragma unroll
+  for (int st = 0; st < NSET; ++st) {
+    const int iq = (n / 4) % QS + 4 * st;
+    const uint4 *q4 = reinterpret_cast<const uint4 *>(A.q + (int64_t)(qh0 + iq) * kHeadDim + 32 * a);
+    uint4 qr[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) qr[j] = q4[j];
+    float qf[32];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t w[4] = {qr[j].x, qr[j].y, qr[j].z, qr[j].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        qf[8 * j + 2 * k] = f16_to_f32((uint16_t)(w[k] & 0xffffu));
+        qf[8 * j + 2 * k + 1] = f16_to_f32((uint16_t)(w[k] >> 16));
+      }
+    }
+    if constexpr (SPLITQ) {
+      const float4 *b4 = reinterpret_cast<const float4 *>(A.balance + (int64_t)h * kHeadDim + 32 * a);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float4 v = b4[j];
+        qf[4 * j] = qf[4 * j] / v.x;
+        qf[4 * j + 1] = qf[4 * j + 1] / v.y;
+        qf[4 * j + 2] = qf[4 * j + 2] / v.z;
+        qf[4 * j + 3] = qf[4 * j + 3] / v.w;
+      }
+    }
+    float ps = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) ps += qf[j];
+    qpart[st] = ps;
+    const float keep = (32 * a) / GROUP == n % 4 ? 1.0f : 0.0f;  // the lane's channels lie in one group
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      uint32_t hw[4], lw[4];
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        float vv[2];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int e = 2 * d + hf;
+          const int j = 16 * (i >> 1) + 4 * (i & 1) + (e >> 1) + 8 * (e & 1);
+          vv[hf] = qf[j] * (keep * __builtin_ldexpf(1.0f, -2 * (e >> 1)));
+        }
+        const _Float16 h0 = (_Float16)vv[0], h1 = (_Float16)vv[1];
+        hw[d] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+        if constexpr (SPLITQ) {
+          const _Float16 l0 = (_Float16)(vv[0] - (float)h0), l1 = (_Float16)(vv[1] - (float)h1);
+          lw[d] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+        }
+      }
+      AK[st][0][i] = pack_h8(hw[0], hw[1], hw[2], hw[3]);
+      if constexpr (SPLITQ) AK[st][NP - 1][i] = pack_h8(lw[0], lw[1], lw[2], lw[3]);
+    }
+  }
+  // Sum of q_hat over each group for the lane's own query slot (the zero
+  // term of the folded dequantization), from the rows 4 s of lane groups a'.
+  float qsl[NSET][NG];
+#pragma unroll
+  for (int st = 0; st < NSET; ++st) {
+    float all[QS][NG];
+#pragma unroll
+    for (int s3 = 0; s3 < QS; ++s3) {
+#pragma unroll
+      for (int gm = 0; gm < NG; ++gm) all[s3][gm] = 0.0f;
+#pragma unroll
+      for (int ap = 0; ap < 4; ++ap) all[s3][(32 * ap) / GROUP] += lane_value(qpart[st], 16 * ap + 4 * s3);
+    }
+#pragma unroll
+    for (int gm = 0; gm < NG; ++gm) {
+      float v = all[0][gm];
+#pragma unroll
+      for (int s3 = 1; s3 < QS; ++s3) v = qs == s3 ? all[s3][gm] : v;
+      qsl[st][gm] = v;
+    }
+  }
+
+  float m2q[G];       // running max per query (wave-uniform, log2 units)
+  float m_own[NSET];  // the max of the lane's own query
+#pragma unroll
+  for (int i = 0; i < G; ++i) m2q[i] = kNegInf;
+#pragma unroll
+  for (int st = 0; st < NSET; ++st) m_own[st] = kNegInf;
+  float l_l[NSET], bs_l[NSET][NGL];
+#pragma unroll
+  for (int st = 0; st < NSET; ++st) {
+    l_l[st] = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NGL; ++j) bs_l[st][j] = 0.0f;
+  }
+  // a lane's duplicate value group (fewer groups than replicas) adds nothing
+  float dup[NGL];
+#pragma unroll
+  for (int j = 0; j < NGL; ++j) dup[j] = rho + R * j < NG ? 1.0f : 0.0f;
+  f4_t CV[8];
+#pragma unroll
+  for (int nb = 0; nb < 8; ++nb) CV[nb] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  const uint32_t mk = 0x00030003u << (2 * (n & 3));  // value field of this lane's column
+
+  for (int it = 0; it < n_iter; ++it) {
+    if (it > 0) load(cur, it);
+    const int t0 = start + it * kItTok;
+    // --- scores of the four key tiles
+    float s2[4][NSET];
+    bool raise = false;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t P[16];
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const uint32_t x = cur.kc[q][w], y = x >> 8;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          P[(2 * w) * 4 + k] = x & (0x00030003u << (2 * k));
+          P[(2 * w + 1) * 4 + k] = y & (0x00030003u << (2 * k));
+        }
+      }
+      const bool valid = t0 + 16 * q + n < end;
+#pragma unroll
+      for (int st = 0; st < NSET; ++st) {
+        f4_t C = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int pt = 0; pt < NP; ++pt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            C = mfma32(AK[st][pt][i], pack_h8(P[4 * i], P[4 * i + 1], P[4 * i + 2], P[4 * i + 3]), C);
+        float s = 0.0f;
+#pragma unroll
+        for (int gm = 0; gm < NG; ++gm) {
+          const uint32_t kw = cur.kp[q][gm];
+          const float ka = __builtin_ldexpf(f16_to_f32((uint16_t)(kw & 0xffffu)), 24);
+          s = fmaf(ka, C[gm], fmaf(f16_to_f32((uint16_t)(kw >> 16)), qsl[st][gm], s));
+        }
+        const float v2 = valid ? s * s2scale : kNegInf;
+        s2[q][st] = v2;
+        if (scores) s_lds[(qs + 4 * st) * kMaxChunk + (t0 - start) + 16 * q + n] = v2;  // replicas agree
+        raise = raise || (v2 > m_own[st] + kLazy);
+      }
+    }
+    // --- lazy running max (per query; rare after the first tokens)
+    if (__ballot(raise)) {
+      float f[G];
+#pragma unroll
+      for (int i = 0; i < G; ++i) f[i] = 1.0f;
+#pragma unroll
+      for (int st = 0; st < NSET; ++st) {
+        float mx = fmaxf(fmaxf(s2[0][st], s2[1][st]), fmaxf(s2[2][st], s2[3][st]));
+        mx = row_max16(mx);
+        float ra[4];
+#pragma unroll
+        for (int ap = 0; ap < 4; ++ap) ra[ap] = lane_value(mx, 16 * ap);
+#pragma unroll
+        for (int s3 = 0; s3 < QS; ++s3) {
+          float qm = kNegInf;
+#pragma unroll
+          for (int ap = 0; ap < 4; ++ap)
+            if (ap % QS == s3) qm = fmaxf(qm, ra[ap]);
+          const int iq = s3 + 4 * st;
+          if (qm > m2q[iq]) {
+            f[iq] = m2q[iq] == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(m2q[iq] - qm);
+            m2q[iq] = qm;
+          }
+        }
+      }
+#pragma unroll
+      for (int st = 0; st < NSET; ++st) {
+        float fo = f[4 * st], mo = m2q[4 * st];
+#pragma unroll
+        for (int s3 = 1; s3 < QS; ++s3) {
+          fo = qs == s3 ? f[s3 + 4 * st] : fo;
+          mo = qs == s3 ? m2q[s3 + 4 * st] : mo;
+        }
+        m_own[st] = mo;
+        l_l[st] *= fo;
+#pragma unroll
+        for (int j = 0; j < NGL; ++j) bs_l[st][j] *= fo;
+      }
+      // value accumulators: register r of lane group a is row 4a + r, query (4a + r) / 2
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float fr = 1.0f;
+#pragma unroll
+        for (int i = 0; i < G; ++i) fr = (4 * a + r) / 2 == i ? f[i] : fr;
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) CV[nb][r] *= fr;
+      }
+    }
+    // --- weights e * alpha into LDS (the A layout of the value MFMAs)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int p = 16 * q + n, vt = p >> 5, u = p & 31;
+      const int gv = u >> 3, ei = tau8(u & 7);
+#pragma unroll
+      for (int st = 0; st < NSET; ++st) {
+        const int iq = qs + 4 * st;
+        const float e = __builtin_amdgcn_exp2f(s2[q][st] - m_own[st]);  // 0 for -inf scores
+        l_l[st] += e;
+#pragma unroll
+        for (int j = 0; j < NGL; ++j) {
+          const int gm = (rho + R * j) % NG;
+          const uint32_t vpw = cur.vp[q][j];
+          const float w = e * f16_to_f32((uint16_t)(vpw & 0xffffu));
+          bs_l[st][j] = fmaf(e * dup[j], f16_to_f32((uint16_t)(vpw >> 16)), bs_l[st][j]);
+          const _Float16 wh = (_Float16)w, wl = (_Float16)(w - (float)wh);
+          w_lds[w_index(gm, vt, 2 * iq, gv, ei)] = wh;
+          w_lds[w_index(gm, vt, 2 * iq + 1, gv, ei)] = wl;
+        }
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // --- value MFMAs
+#pragma unroll
+    for (int vt = 0; vt < 2; ++vt) {
+      h8_t AV[NG];
+#pragma unroll
+      for (int gm = 0; gm < NG; ++gm) AV[gm] = *reinterpret_cast<const h8_t *>(w_lds + w_index(gm, vt, n, a, 0));
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) {
+        const uint32_t d0 = cur.vc[vt][nb][0], d1 = cur.vc[vt][nb][1];
+        CV[nb] = mfma32(AV[(16 * nb) / GROUP], pack_h8(d0 & mk, (d0 >> 8) & mk, d1 & mk, (d1 >> 8) & mk), CV[nb]);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+
+  // Scores of the chunk: one burst from LDS.
+  const int nc = A.nc_hi + A.nc_lo;
+  if (scores) {
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      float *row = scores + (int64_t)(qh0 + i) * cap;
+      for (int j = lane; j < end - start; j += 64) row[start + j] = s_lds[i * kMaxChunk + j];
+    }
+  }
+  // Normalisers and zero terms per (query, group), wave-uniform.
+  float lq[G], bq[G][NG];
+#pragma unroll
+  for (int st = 0; st < NSET; ++st) {
+    const float lr = row_sum16(l_l[st]);
+    float br[NGL];
+#pragma unroll
+    for (int j = 0; j < NGL; ++j) br[j] = row_sum16(bs_l[st][j]);
+#pragma unroll
+    for (int s3 = 0; s3 < QS; ++s3) {
+      const int iq = s3 + 4 * st;
+      lq[iq] = lane_value(lr, 16 * s3);  // replica 0 of the slot
+#pragma unroll
+      for (int gm = 0; gm < NG; ++gm) bq[iq][gm] = lane_value(br[gm / R], 16 * (s3 + QS * (gm % R)));
+    }
+  }
+  // Record per query: max, normaliser, value sums (lane group i/2 holds
+  // query i in registers 2(i%2), 2(i%2)+1).
+  const float colscale = __builtin_ldexpf(1.0f, 24 - 2 * (n & 3));
+#pragma unroll
+  for (int i = 0; i < G; ++i) {
+    float *rec = A.partials + ((int64_t)(qh0 + i) * nc + rec_chunk) * kRec;
+    if (lane == 0) {
+      rec[0] = m2q[i];
+      rec[1] = lq[i];
+    }
+    if (a == i / 2) {
+      const int r0 = 2 * (i % 2);
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb) rec[kRecO + 16 * nb + n] = fmaf(CV[nb][r0] + CV[nb][r0 + 1], colscale, bq[i][(16 * nb) / GROUP]);
+    }
+  }
+}
+
 // Tuning: token tiles per lane per iteration and prefetch depth, for
 // low-bit (INT2/INT4) and high-bit (fp16/INT8) rows.
 #ifndef MIKV_UNROLL_LOWBIT
@@ -504,6 +918,11 @@ constexpr int unroll_for() { return BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL
 template <int BITS>
 constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PREFETCH_HIGHBIT; }
 
+// Query heads per KV head from which a lane holds 16 channels instead of 32
+// (fewer accumulators per lane at larger GQA groups).
+#ifndef MIKV_NARROW_FROM_G
+#define MIKV_NARROW_FROM_G 8
+#endif
 #ifndef MIKV_WAVES_PER_EU
 #define MIKV_WAVES_PER_EU 1
 #endif
@@ -514,13 +933,22 @@ constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PR
 template <int HI, int LO, int G, bool SPLITQ>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
-  constexpr int CPL = G == 8 ? 16 : 32;
+  constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
   const int h = blockIdx.y, c = blockIdx.x;
   __shared__ float s_lds[G * kMaxChunk];  // the chunk's scores, [G][kMaxChunk]
-  if (c < A.nc_hi)
+  if (c < A.nc_hi) {
     attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
-  else
+  } else if constexpr (LO == 2 && G >= 2) {
+    __shared__ __align__(16) _Float16 w_lds[kWLds];  // value-MFMA weights, see w_index
+    if (A.group == 32)
+      attn_chunk_int2<G, SPLITQ, 4>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+    else if (A.group == 64)
+      attn_chunk_int2<G, SPLITQ, 2>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+    else
+      attn_chunk_int2<G, SPLITQ, 1>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+  } else {
     attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
+  }
 }
 
 // Softmax over the whole sequence from the chunk records (Section 2.1): a

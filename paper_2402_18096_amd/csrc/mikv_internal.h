@@ -113,6 +113,33 @@ __device__ inline uint32_t encode(float x, const GroupParams &p, int bits) {
 }
 
 // ---------------------------------------------------------------------------
+// Retained-pool 2-bit value codes for GQA: tiles of 32 slots, quad-major.
+// A slot's LSB-first packed 2-bit row has 32 bytes; byte q holds channels
+// 4q..4q+3.  In a tiled value array that byte of slot s sits at (s / 32) * 1024 + 32 * q + (s % 32): the same channel quad
+// of 32 consecutive slots is contiguous, the operand shape the decode
+// attention's matrix cores read (tokens along the reduction).  Every byte
+// belongs to one slot, so slots are written independently.
+// ---------------------------------------------------------------------------
+// The tiled value layout is used where the matrix cores read it: 2-bit
+// retained pools shared by two or more query heads (GQA).  With one query
+// head per KV head the values stay token-major (the vector path reads a
+// token's row per lane).
+__host__ __device__ inline bool int2_values_tiled(int lo_bits, int q_heads, int kv_heads) {
+  return lo_bits == 2 && q_heads >= 2 * kv_heads;
+}
+
+__host__ __device__ inline int64_t int2_v_byte(int64_t slot, int quad) {
+  return (slot >> 5) * 1024 + (int64_t)quad * 32 + (slot & 31);
+}
+
+// Store the 8 packed bytes of channels [32 * part, 32 * part + 32) of a
+// slot's 2-bit value row (two little-endian words) into the tiled layout.
+__device__ inline void store_int2_v(uint8_t *head_base, int64_t slot, int part, const uint32_t w[2]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) head_base[int2_v_byte(slot, 8 * part + j)] = (uint8_t)((w[j >> 2] >> (8 * (j & 3))) & 0xffu);
+}
+
+// ---------------------------------------------------------------------------
 // Device: wave-level reductions (wave64).
 // ---------------------------------------------------------------------------
 template <int WIDTH>

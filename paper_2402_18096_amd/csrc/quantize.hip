@@ -34,12 +34,11 @@ __device__ inline void load_row_segment(const uint16_t *src, const float *bal, f
   }
 }
 
-// Quantize one 32-channel segment (lane part `lane4` of its row) at BITS,
-// group size `group`: writes the packed codes (32*BITS/8 bytes at `codes`)
-// and, from the first lane of each group, the (alpha, beta) pair at `param`.
+// Eq. 1 codes of one 32-channel segment at BITS: group min/max (a group of
+// g channels spans g/32 adjacent lanes, combined with shuffles), the group's
+// fp16 (alpha, beta) and the packed little-endian words w[BITS].
 template <int BITS>
-__device__ inline void quantize_segment(const float x[32], int group, int lane4, uint8_t *codes,
-                                        uint32_t *param, bool store) {
+__device__ inline GroupParams quantize_words(const float x[32], int group, uint32_t w[BITS]) {
   float mn = x[0], mx = x[0];
 #pragma unroll
   for (int c = 1; c < 32; ++c) {
@@ -52,16 +51,25 @@ __device__ inline void quantize_segment(const float x[32], int group, int lane4,
     mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   }
   GroupParams p = group_params(mn, mx, BITS);
-  constexpr int kWords = 32 * BITS / 32;
-  uint32_t w[kWords];
 #pragma unroll
-  for (int i = 0; i < kWords; ++i) w[i] = 0u;
+  for (int i = 0; i < BITS; ++i) w[i] = 0u;
 #pragma unroll
   for (int c = 0; c < 32; ++c) w[(c * BITS) / 32] |= encode(x[c], p, BITS) << ((c * BITS) % 32);
+  return p;
+}
+
+// Quantize one 32-channel segment (lane part `lane4` of its row) at BITS:
+// writes the packed codes (32*BITS/8 bytes at `codes`) and, from the first
+// lane of each group, the (alpha, beta) pair at `param`.
+template <int BITS>
+__device__ inline void quantize_segment(const float x[32], int group, int lane4, uint8_t *codes,
+                                        uint32_t *param, bool store) {
+  uint32_t w[BITS];
+  GroupParams p = quantize_words<BITS>(x, group, w);
   if (!store) return;
   uint32_t *dst = reinterpret_cast<uint32_t *>(codes);
 #pragma unroll
-  for (int i = 0; i < kWords; ++i) dst[i] = w[i];
+  for (int i = 0; i < BITS; ++i) dst[i] = w[i];
   if ((lane4 % (group / 32)) == 0) *param = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
 }
 
@@ -96,6 +104,7 @@ struct Pools {
   uint8_t *map;
   int32_t *status;
   int cap_hi, cap_lo, max_len, group;
+  int v_tiled;  // 2-bit values in the tiled layout (int2_values_tiled)
 };
 
 Pools make_pools(const mikv_cache *c) {
@@ -119,6 +128,7 @@ Pools make_pools(const mikv_cache *c) {
   p.cap_lo = c->cap_lo;
   p.max_len = c->max_len;
   p.group = c->group;
+  p.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
   return p;
 }
 
@@ -252,6 +262,16 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
         uint8_t *dst = (is_v ? P.hi_v : P.hi_k) + ((int64_t)h * P.cap_hi + sl) * kHeadDim + lane4 * 32;
         uint32_t *par = (is_v ? P.hi_vp : P.hi_kp) + ((int64_t)h * P.cap_hi + sl) * ng + (lane4 * 32) / P.group;
         quantize_segment<8>(x, P.group, lane4, dst, par, store);
+      }
+    } else if (LO_BITS == 2 && is_v && P.v_tiled) {
+      // 2-bit values of a GQA cache go to the tiled layout, byte by byte
+      uint32_t w[2];
+      GroupParams gp = quantize_words<2>(x, P.group, w);
+      if (store) {
+        store_int2_v(P.lo_v + (int64_t)h * P.cap_lo * (kHeadDim / 4), sl, lane4, w);
+        if ((lane4 % (P.group / 32)) == 0)
+          P.lo_vp[((int64_t)h * P.cap_lo + sl) * ng + (lane4 * 32) / P.group] =
+              (uint32_t)gp.a16 | ((uint32_t)gp.b16 << 16);
       }
     } else {
       uint8_t *dst = (is_v ? P.lo_v : P.lo_k) + ((int64_t)h * P.cap_lo + sl) * (kHeadDim * LO_BITS / 8) +

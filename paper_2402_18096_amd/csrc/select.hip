@@ -132,6 +132,7 @@ struct SelArgs {
   int32_t *ws;
   int cap_hi, cap_lo, max_len, group;
   int length, k_heavy, window;
+  int v_tiled;  // 2-bit values in the tiled layout (int2_values_tiled)
 };
 
 // Decode the 32 channels [part*32, part*32+32) of an importance-pool row.
@@ -164,10 +165,10 @@ __device__ inline void load_hi_segment(const SelArgs &A, const uint8_t *rows, co
   }
 }
 
-// Eq. 1 at LO_BITS of 32 decoded channels; group spans group/32 lanes.
+// Eq. 1 codes at LO_BITS of 32 decoded channels (a group spans group/32
+// lanes): the packed little-endian words and the group parameters.
 template <int LO_BITS>
-__device__ inline void store_lo_segment(const SelArgs &A, uint8_t *codes, uint32_t *par, int part, const float x[32],
-                                        bool store) {
+__device__ inline GroupParams lo_words(const SelArgs &A, const float x[32], uint32_t w[LO_BITS]) {
   float mn = x[0], mx = x[0];
 #pragma unroll
   for (int c = 1; c < 32; ++c) {
@@ -179,34 +180,44 @@ __device__ inline void store_lo_segment(const SelArgs &A, uint8_t *codes, uint32
     mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   }
   GroupParams p = group_params(mn, mx, LO_BITS);
-  constexpr int kWords = LO_BITS;  // 32 channels * LO_BITS bits / 32
-  uint32_t w[kWords];
 #pragma unroll
-  for (int i = 0; i < kWords; ++i) w[i] = 0u;
+  for (int i = 0; i < LO_BITS; ++i) w[i] = 0u;
 #pragma unroll
   for (int c = 0; c < 32; ++c) w[(c * LO_BITS) / 32] |= encode(x[c], p, LO_BITS) << ((c * LO_BITS) % 32);
-  if (!store) return;
-#pragma unroll
-  for (int i = 0; i < kWords; ++i) reinterpret_cast<uint32_t *>(codes)[i] = w[i];
-  if ((part % (A.group / 32)) == 0) *par = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
+  return p;
 }
 
-// Requantize importance-pool slot `slot` (K and V rows) into retained-pool
-// slot `lslot`; threads [0, 8) of the block take part (4 lanes per row).
+// Eq. 1 at LO_BITS of 32 decoded channels into retained-pool slot lslot:
+// codes token-major, except 2-bit values of a GQA cache (tiled layout).
+template <int LO_BITS>
+__device__ inline void store_lo_segment(const SelArgs &A, int h, int64_t lslot, bool is_v, int part,
+                                        const float x[32]) {
+  const int ng = kHeadDim / A.group;
+  uint32_t w[LO_BITS];
+  GroupParams p = lo_words<LO_BITS>(A, x, w);
+  if (LO_BITS == 2 && is_v && A.v_tiled) {
+    store_int2_v(A.lo_v + (int64_t)h * A.cap_lo * (kHeadDim / 4), lslot - (int64_t)h * A.cap_lo, part, w);
+  } else {
+    uint32_t *codes = reinterpret_cast<uint32_t *>((is_v ? A.lo_v : A.lo_k) + lslot * (kHeadDim * LO_BITS / 8) +
+                                                   part * (32 * LO_BITS / 8));
+#pragma unroll
+    for (int i = 0; i < LO_BITS; ++i) codes[i] = w[i];
+  }
+  if ((part % (A.group / 32)) == 0)
+    (is_v ? A.lo_vp : A.lo_kp)[lslot * ng + (part * 32) / A.group] = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
+}
+
 template <int HI_BITS, int LO_BITS>
 __device__ inline void demote_row(const SelArgs &A, int h, int slot, int64_t lslot, int p) {
   if (threadIdx.x >= 8) return;
   const int ng = kHeadDim / A.group;
   const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
-  const int64_t lrow = kHeadDim * LO_BITS / 8;
   const int is_v = threadIdx.x >> 2, part = threadIdx.x & 3;
   const uint8_t *rows = (is_v ? A.hi_v : A.hi_k) + (int64_t)h * A.cap_hi * hrow;
   const uint32_t *pars = HI_BITS == 16 ? nullptr : (is_v ? A.hi_vp : A.hi_kp) + (int64_t)h * A.cap_hi * ng;
   float x[32];
   load_hi_segment<HI_BITS>(A, rows, pars, slot, part, x);
-  uint8_t *codes = (is_v ? A.lo_v : A.lo_k) + lslot * lrow + part * (32 * LO_BITS / 8);
-  uint32_t *par = (is_v ? A.lo_vp : A.lo_kp) + lslot * ng + (part * 32) / A.group;
-  store_lo_segment<LO_BITS>(A, codes, par, part, x, true);
+  store_lo_segment<LO_BITS>(A, h, lslot, is_v, part, x);
   if (threadIdx.x == 0) {
     A.lo_pos[lslot] = p;
     if (A.map) A.map[(int64_t)h * A.max_len + p] = 0;
@@ -350,7 +361,6 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
   // re-quantize the demoted tokens into the retained pool (4 lanes per row)
   const int ng = kHeadDim / A.group;
   const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
-  const int64_t lrow = kHeadDim * LO_BITS / 8;
   for (int r = threadIdx.x >> 2; r < 2 * n_dem; r += kSel / 4) {
     const int d = r >> 1, is_v = r & 1, part = threadIdx.x & 3;
     const int slot = dem_list[d];
@@ -359,9 +369,7 @@ __global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
     float x[32];
     load_hi_segment<HI_BITS>(A, rows, pars, slot, part, x);
     const int64_t lslot = (int64_t)h * A.cap_lo + n_lo0 + d;
-    uint8_t *codes = (is_v ? A.lo_v : A.lo_k) + lslot * lrow + part * (32 * LO_BITS / 8);
-    uint32_t *par = (is_v ? A.lo_vp : A.lo_kp) + lslot * ng + (part * 32) / A.group;
-    store_lo_segment<LO_BITS>(A, codes, par, part, x, true);
+    store_lo_segment<LO_BITS>(A, h, lslot, is_v, part, x);
     if (part == 0 && !is_v) {
       const int p = pos[slot];
       A.lo_pos[lslot] = p;
@@ -471,6 +479,7 @@ extern "C" int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_h
   A.length = length;
   A.k_heavy = k_heavy;
   A.window = window;
+  A.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
   const int NH = n_heads_of(c);
   hipStream_t st = (hipStream_t)stream;
   switch (c->hi_bits * 100 + c->lo_bits) {

@@ -119,10 +119,16 @@ def _workspace(nbytes: int, device) -> torch.Tensor:
 # -- cache ------------------------------------------------------------------------
 
 class MikvCache:
-    """Device buffers of one mixed-precision cache (see ``struct mikv_cache``)."""
+    """Device buffers of one mixed-precision cache (see ``struct mikv_cache``).
+
+    A 2-bit retained pool shared by several query heads keeps its value codes
+    in tiles of 32 slots, so its capacity is rounded up to a multiple of 32."""
 
     def __init__(self, batch: int, q_heads: int, kv_heads: int, group: int, hi_bits: int, lo_bits: int,
                  cap_hi: int, cap_lo: int, max_len: int, device="cuda", with_map: bool = True):
+        self.values_tiled = lo_bits == 2 and q_heads >= 2 * kv_heads
+        if self.values_tiled:
+            cap_lo = (cap_lo + 31) // 32 * 32
         self.batch, self.q_heads, self.kv_heads = batch, q_heads, kv_heads
         self.group, self.hi_bits, self.lo_bits = group, hi_bits, lo_bits
         self.cap_hi, self.cap_lo, self.max_len = cap_hi, cap_lo, max_len

@@ -39,6 +39,16 @@ def np16(t: torch.Tensor) -> np.ndarray:
     return t.detach().cpu().contiguous().numpy().view(np.float16)
 
 
+def int2_values_token_major(v: np.ndarray, cap: int) -> np.ndarray:
+    """Retained-pool 2-bit value codes [NH, cap, 32] in the tiled layout
+    (byte (slot, quad) at slot//32 * 1024 + 32 * quad + slot % 32) back to
+    LSB-first token-major rows."""
+    slot = np.arange(cap)[:, None]
+    quad = np.arange(32)[None, :]
+    idx = (slot // 32) * 1024 + 32 * quad + slot % 32
+    return v.reshape(v.shape[0], -1)[:, idx]
+
+
 def gather_gpu_state(c: mikv.MikvCache):
     """Position-indexed copy of the GPU cache: dict of numpy arrays [NH, L...]."""
     n_hi = c.n_hi.cpu().numpy()
@@ -49,6 +59,8 @@ def gather_gpu_state(c: mikv.MikvCache):
     hv = c.hi_v.cpu().numpy().view(np.uint16 if c.hi_bits == 16 else np.uint8)
     acc = c.hi_acc.cpu().numpy()
     lk, lv = c.lo_k.cpu().numpy(), c.lo_v.cpu().numpy()
+    if c.values_tiled:
+        lv = int2_values_token_major(lv, c.cap_lo)
     lkp = c.lo_kp.cpu().numpy().view(np.uint16)
     lvp = c.lo_vp.cpu().numpy().view(np.uint16)
     hkp = c.hi_kp.cpu().numpy().view(np.uint16) if c.hi_kp is not None else None

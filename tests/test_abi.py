@@ -30,7 +30,7 @@ def test_every_declared_symbol_is_exported():
 
 
 def _desc(**kw):
-    d = dict(batch=1, q_heads=4, kv_heads=4, head_dim=128, group=32, hi_bits=16, lo_bits=2, cap_hi=8, cap_lo=8,
+    d = dict(batch=1, q_heads=4, kv_heads=4, head_dim=128, group=32, hi_bits=16, lo_bits=2, cap_hi=8, cap_lo=32,
              max_len=16)
     d.update(kw)
     c = mikv.CacheDesc()
@@ -56,6 +56,16 @@ def test_cache_validation_errors(field, value, code):
     c = _desc(**{field: value})
     assert _call_attention(c) == code
     assert mikv.lib().mikv_last_error()
+
+
+def test_two_bit_gqa_pool_capacity_multiple_of_32():
+    """2-bit retained pools shared by query heads store values in 32-slot
+    tiles (validation only: every call in this file fails before any
+    launch); with one query head per KV head any capacity is accepted by
+    validation (the call then fails on the workspace)."""
+    assert _call_attention(_desc(q_heads=8, kv_heads=4, cap_lo=48)) == 1
+    assert "multiple of 32" in mikv.lib().mikv_last_error().decode()
+    assert _call_attention(_desc(cap_lo=48), ws_bytes=16) == 3
 
 
 def test_gqa_group_must_be_power_of_two_up_to_8():
@@ -85,7 +95,7 @@ def test_null_pointers_and_capacity():
 
 def test_workspace_sizes_are_consistent():
     L = mikv.lib()
-    c = _desc(cap_hi=100, cap_lo=1000, max_len=1000)
+    c = _desc(cap_hi=100, cap_lo=1024, max_len=1000)
     a = L.mikv_decode_workspace_size(ctypes.byref(c), 500)
     assert a >= 4 * 4 * 100   # at least the scores scratch of the importance pool
     assert L.mikv_select_workspace_size(ctypes.byref(c)) == 2 * 4 * 1 * 4 * 100

@@ -195,7 +195,7 @@ def test_lockstep_single_pool(ratio):
 
 def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
     dev = _dev()
-    c = mikv.MikvCache(1, 2, 2, 32, 16, 2, cap_hi=4, cap_lo=8, max_len=64, device=dev)
+    c = mikv.MikvCache(1, 2, 2, 32, 16, 2, cap_hi=4, cap_lo=32, max_len=64, device=dev)
     k = torch.randn(1, 2, 6, 128, device=dev).half()
     mikv.mikv_quantize_kv(c, k, k.clone(), 0)    # six tokens into a 4-slot importance pool
     torch.cuda.synchronize()
