@@ -256,10 +256,16 @@ int mikv_select_prefill(const float *scores, int32_t n_heads, int32_t length, in
  *   4. mikv_select_topk(k_heavy, window).
  *   q fp16 [B, Hq, 128]; k_new, v_new fp16 [B, Hkv, 128]; other arguments as
  *   in the calls above (probs_hi is required unless MIKV_ATTN_ACCUMULATE).
- *   workspace    at least mikv_decode_step_workspace_size(c, length) bytes;
+ * With MIKV_ATTN_ACCUMULATE and at most 512 (sequence, KV head) pairs,
+ * steps 2 (finalize phase), 3 and 4 run as one launch: the block that
+ * updates a head's importance scores then runs that head's re-rank.
+ *   workspace    at least mikv_decode_step_workspace_size(c, length) bytes
+ *                (the attention's and the select's workspaces); its
+ *                contents need not be initialised;
  *   phase_events NULL, or 6 hipEvent_t (entries may be NULL) recorded on
  *                `stream` before step 1 and after steps 1, 2 (partial
- *                phase), 2 (finalize phase), 3 and 4, for profiling.
+ *                phase), 2 (finalize phase), 3 and 4, for profiling (with
+ *                the fused launch the last three mark its end).
  * Errors: those of the four calls, checked before the first launch where the
  * host can check them.
  */

@@ -35,6 +35,7 @@
 #include <algorithm>
 
 #include "mikv_internal.h"
+#include "select_device.h"
 
 namespace mikv {
 
@@ -993,6 +994,97 @@ __device__ inline void head_stats(const AttnArgs &A, int qh0, int nc, float M[G]
   }
 }
 
+// One probability tile (kProbTile scores of every query head of KV head h):
+// loaded first, so that the latency overlaps the statistics, then stored.
+template <int G>
+struct ProbTile {
+  static constexpr int kPer = kProbTile / kBlock;
+  float sv[kPer][G], a[kPer];
+  int t[kPer];
+  int n_pool;
+};
+
+template <int G>
+__device__ inline ProbTile<G> prob_tile_load(const AttnArgs &A, int h, int qh0, bool is_hi, int tile, bool has_tile,
+                                             bool accumulate) {
+  ProbTile<G> T;
+  const int cap = is_hi ? A.cap_hi : A.cap_lo;
+  const float *scores = is_hi ? A.scores_hi : A.scores_lo;
+  const float *acc = is_hi && accumulate ? A.acc : nullptr;
+#pragma unroll
+  for (int u = 0; u < ProbTile<G>::kPer; ++u) {
+    T.t[u] = tile * kProbTile + u * kBlock + threadIdx.x;
+    const bool ok = has_tile && T.t[u] < cap;
+#pragma unroll
+    for (int i = 0; i < G; ++i) T.sv[u][i] = ok ? scores[(int64_t)(qh0 + i) * cap + T.t[u]] : 0.0f;
+    T.a[u] = ok && acc ? acc[(int64_t)h * A.cap_hi + T.t[u]] : 0.0f;
+  }
+  T.n_pool = has_tile ? (is_hi ? A.n_hi[h] : A.n_lo[h]) : 0;
+  return T;
+}
+
+template <int G>
+__device__ inline void prob_tile_store(const AttnArgs &A, int h, int qh0, bool is_hi, bool accumulate,
+                                       const ProbTile<G> &T, const float M[G], const float inv[G]) {
+  const int cap = is_hi ? A.cap_hi : A.cap_lo;
+  float *probs = is_hi ? A.probs_hi : A.probs_lo;
+  float *acc = is_hi && accumulate ? A.acc : nullptr;
+#pragma unroll
+  for (int u = 0; u < ProbTile<G>::kPer; ++u) {
+    if (T.t[u] >= T.n_pool) continue;
+    float sum = 0.0f;
+#pragma unroll
+    for (int i = 0; i < G; ++i) {
+      const float p = __builtin_amdgcn_exp2f(T.sv[u][i] - M[i]) * inv[i];
+      if (probs) probs[(int64_t)(qh0 + i) * cap + T.t[u]] = p;
+      sum = i == 0 ? p : sum + p;
+    }
+    if (acc) acc[(int64_t)h * A.cap_hi + T.t[u]] = T.a[u] + sum;
+  }
+}
+
+// Output merge of the G query heads (whole block): thread -> (record split
+// s, query head i, 4 channels q4), partial sums reduced in LDS.
+template <int G>
+__device__ inline void merge_output(const AttnArgs &A, int qh0, int nc, const float M[G], const float inv[G]) {
+  constexpr int S = 8 / G;
+  const int q4 = threadIdx.x % 32, i = (threadIdx.x / 32) % G, s = threadIdx.x / (32 * G);
+  const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
+  float Mi = M[0], invi = inv[0];
+#pragma unroll
+  for (int j = 1; j < G; ++j)
+    if (i == j) {
+      Mi = M[j];
+      invi = inv[j];
+    }
+  float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll 4
+  for (int r = s; r < nc; r += S) {
+    const float *rr = rec + (int64_t)r * kRec;
+    const float mr = rr[0];
+    const float4 o = reinterpret_cast<const float4 *>(rr + kRecO)[q4];
+    const float w = mr == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(mr - Mi);
+    v.x = fmaf(o.x, w, v.x);
+    v.y = fmaf(o.y, w, v.y);
+    v.z = fmaf(o.z, w, v.z);
+    v.w = fmaf(o.w, w, v.w);
+  }
+  __shared__ float4 s_o[kBlock];
+  s_o[threadIdx.x] = v;
+  __syncthreads();
+  if (s == 0) {
+    for (int s2 = 1; s2 < S; ++s2) {
+      const float4 u = s_o[threadIdx.x + s2 * 32 * G];
+      v.x += u.x;
+      v.y += u.y;
+      v.z += u.z;
+      v.w += u.w;
+    }
+    reinterpret_cast<float4 *>(A.out + (int64_t)(qh0 + i) * kHeadDim)[q4] =
+        make_float4(v.x * invi, v.y * invi, v.z * invi, v.w * invi);
+  }
+}
+
 template <int G>
 __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi,
                                                                int tiles_lo) {
@@ -1000,84 +1092,49 @@ __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int a
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
-
-  // Probability tile of this block: its scores (and importance scores) are
-  // loaded first, so that their latency overlaps the statistics below.
   const bool is_hi = c < tiles_hi;
   const bool has_tile = is_hi || c - tiles_hi < tiles_lo;
-  const int tile = is_hi ? c : c - tiles_hi;
-  const int cap = is_hi ? A.cap_hi : A.cap_lo;
-  const float *scores = is_hi ? A.scores_hi : A.scores_lo;
-  float *probs = is_hi ? A.probs_hi : A.probs_lo;
-  float *acc = is_hi && accumulate ? A.acc : nullptr;
-  constexpr int kPer = kProbTile / kBlock;
-  float sv[kPer][G], a[kPer];
-  int t[kPer];
-#pragma unroll
-  for (int u = 0; u < kPer; ++u) {
-    t[u] = tile * kProbTile + u * kBlock + threadIdx.x;
-    const bool ok = has_tile && t[u] < cap;
-#pragma unroll
-    for (int i = 0; i < G; ++i) sv[u][i] = ok ? scores[(int64_t)(qh0 + i) * cap + t[u]] : 0.0f;
-    a[u] = ok && acc ? acc[(int64_t)h * A.cap_hi + t[u]] : 0.0f;
-  }
-  const int n_pool = has_tile ? (is_hi ? A.n_hi[h] : A.n_lo[h]) : 0;
-
+  const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, is_hi, is_hi ? c : c - tiles_hi, has_tile, accumulate);
   float M[G], inv[G];
   head_stats<G>(A, qh0, nc, M, inv);
+  if (c == 0) merge_output<G>(A, qh0, nc, M, inv);
+  if (has_tile) prob_tile_store<G>(A, h, qh0, is_hi, accumulate, T, M, inv);
+}
 
-  if (c == 0) {
-    // Output merge.  Thread -> (record split s, query head i, 4 channels q4).
-    constexpr int S = 8 / G;
-    const int q4 = threadIdx.x % 32, i = (threadIdx.x / 32) % G, s = threadIdx.x / (32 * G);
-    const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
-    float Mi = M[0], invi = inv[0];
-#pragma unroll
-    for (int j = 1; j < G; ++j)
-      if (i == j) {
-        Mi = M[j];
-        invi = inv[j];
-      }
-    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-#pragma unroll 4
-    for (int r = s; r < nc; r += S) {
-      const float *rr = rec + (int64_t)r * kRec;
-      const float mr = rr[0];
-      const float4 o = reinterpret_cast<const float4 *>(rr + kRecO)[q4];
-      const float w = mr == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(mr - Mi);
-      v.x = fmaf(o.x, w, v.x);
-      v.y = fmaf(o.y, w, v.y);
-      v.z = fmaf(o.z, w, v.z);
-      v.w = fmaf(o.w, w, v.w);
-    }
-    __shared__ float4 s_o[kBlock];
-    s_o[threadIdx.x] = v;
-    __syncthreads();
-    if (s == 0) {
-      for (int s2 = 1; s2 < S; ++s2) {
-        const float4 u = s_o[threadIdx.x + s2 * 32 * G];
-        v.x += u.x;
-        v.y += u.y;
-        v.z += u.z;
-        v.w += u.w;
-      }
-      reinterpret_cast<float4 *>(A.out + (int64_t)(qh0 + i) * kHeadDim)[q4] =
-          make_float4(v.x * invi, v.y * invi, v.z * invi, v.w * invi);
-    }
+// Finalize with the importance update and the re-rank fused (the decode
+// step): block 0 of head h merges the output, turns every importance-pool
+// tile into probabilities and score updates, and then, its own writes
+// being the only scores the re-rank reads, runs the head's top-k and
+// demotion; blocks 1.. handle the retained-pool tiles.  No block waits on
+// another.
+template <int G, int HI, int LO>
+__global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int tiles_hi, int tiles_lo, SelArgs S) {
+  const int h = blockIdx.y, c = blockIdx.x;
+  const int b = h / A.kv_heads, kvh = h % A.kv_heads;
+  const int qh0 = b * A.q_heads + kvh * G;
+  const int nc = A.nc_hi + A.nc_lo;
+  if (c > 0) {
+    const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, false, c - 1, c - 1 < tiles_lo, false);
+    float M[G], inv[G];
+    head_stats<G>(A, qh0, nc, M, inv);
+    prob_tile_store<G>(A, h, qh0, false, false, T, M, inv);
+    return;
   }
-
-#pragma unroll
-  for (int u = 0; u < kPer; ++u) {
-    if (t[u] >= n_pool) continue;
-    float sum = 0.0f;
-#pragma unroll
-    for (int i = 0; i < G; ++i) {
-      const float p = __builtin_amdgcn_exp2f(sv[u][i] - M[i]) * inv[i];
-      if (probs) probs[(int64_t)(qh0 + i) * cap + t[u]] = p;
-      sum = i == 0 ? p : sum + p;
-    }
-    if (acc) acc[(int64_t)h * A.cap_hi + t[u]] = a[u] + sum;
+  // the first two importance-pool tiles are in flight with the statistics
+  // and the merge; larger pools continue tile by tile
+  const ProbTile<G> T0 = prob_tile_load<G>(A, h, qh0, true, 0, tiles_hi > 0, true);
+  const ProbTile<G> T1 = prob_tile_load<G>(A, h, qh0, true, 1, tiles_hi > 1, true);
+  float M[G], inv[G];
+  head_stats<G>(A, qh0, nc, M, inv);
+  merge_output<G>(A, qh0, nc, M, inv);
+  if (tiles_hi > 0) prob_tile_store<G>(A, h, qh0, true, true, T0, M, inv);
+  if (tiles_hi > 1) prob_tile_store<G>(A, h, qh0, true, true, T1, M, inv);
+  for (int tile = 2; tile < tiles_hi; ++tile) {
+    const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, true, tile, true, true);
+    prob_tile_store<G>(A, h, qh0, true, true, T, M, inv);
   }
+  __syncthreads();  // the block's score updates are complete before the re-rank reads them
+  select_head<HI, LO>(S, h);
 }
 
 template <int G>
@@ -1209,16 +1266,16 @@ extern "C" size_t mikv_decode_workspace_size(const mikv_cache *c, int32_t length
   return workspace_bytes_for(c, make_plan(c, length));
 }
 
-extern "C" int mikv_decode_attention_partial(const mikv_cache *c, int32_t length, const uint16_t *q,
-                                             const float *balance, float scale, float *out, float *probs_hi,
-                                             float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
-                                             void *stream) {
+namespace mikv {
+
+int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
+                   float *out, float *probs_hi, float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
+                   hipStream_t st) {
   int rc = check_attention_args(c, length, q, balance, out, ws, ws_bytes, "mikv_decode_attention_partial");
   if (rc) return rc;
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, flags, ws);
   dim3 grid(p.nc_hi + p.nc_lo, n_heads_of(c));
-  hipStream_t st = (hipStream_t)stream;
   const int G = group_size_of(c);
   switch (c->hi_bits * 100 + c->lo_bits) {
     case 1602: launch_partial_g<16, 2>(A, G, grid, st); break;
@@ -1229,6 +1286,51 @@ extern "C" int mikv_decode_attention_partial(const mikv_cache *c, int32_t length
     default: launch_partial_g<8, 8>(A, G, grid, st); break;
   }
   return check_launch("mikv_decode_attention_partial");
+}
+
+template <int HI, int LO>
+void launch_finalize_select(const AttnArgs &A, const SelArgs &S, int G, dim3 grid, int tiles_hi, int tiles_lo,
+                            hipStream_t st) {
+  switch (G) {
+    case 1: hipLaunchKernelGGL((finalize_select_kernel<1, HI, LO>), grid, dim3(kBlock), 0, st, A, tiles_hi, tiles_lo, S); break;
+    case 2: hipLaunchKernelGGL((finalize_select_kernel<2, HI, LO>), grid, dim3(kBlock), 0, st, A, tiles_hi, tiles_lo, S); break;
+    case 4: hipLaunchKernelGGL((finalize_select_kernel<4, HI, LO>), grid, dim3(kBlock), 0, st, A, tiles_hi, tiles_lo, S); break;
+    default: hipLaunchKernelGGL((finalize_select_kernel<8, HI, LO>), grid, dim3(kBlock), 0, st, A, tiles_hi, tiles_lo, S); break;
+  }
+}
+
+int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
+                           float *out, float *probs_hi, float *probs_lo, void *ws, size_t ws_bytes, int32_t k_heavy,
+                           int32_t window, void *sel_ws, hipStream_t st) {
+  int rc = check_attention_args(c, length, q, balance, out, ws, ws_bytes, "mikv_decode_step");
+  if (rc) return rc;
+  Plan p = make_plan(c, length);
+  AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, MIKV_ATTN_ACCUMULATE, ws);
+  const SelArgs S = make_sel_args(c, length, k_heavy, window, sel_ws);
+  const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
+  const int tiles_hi = (span_hi + kProbTile - 1) / kProbTile;  // probabilities accumulated
+  const int tiles_lo = A.probs_lo ? (span_lo + kProbTile - 1) / kProbTile : 0;
+  dim3 grid(1 + tiles_lo, n_heads_of(c));  // block 0: output, importance pool, re-rank
+  const int G = group_size_of(c);
+  switch (c->hi_bits * 100 + c->lo_bits) {
+    case 1602: launch_finalize_select<16, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    case 1604: launch_finalize_select<16, 4>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    case 1608: launch_finalize_select<16, 8>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    case 802: launch_finalize_select<8, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    case 804: launch_finalize_select<8, 4>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    default: launch_finalize_select<8, 8>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+  }
+  return check_launch("mikv_decode_step (finalize and select)");
+}
+
+}  // namespace mikv
+
+extern "C" int mikv_decode_attention_partial(const mikv_cache *c, int32_t length, const uint16_t *q,
+                                             const float *balance, float scale, float *out, float *probs_hi,
+                                             float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
+                                             void *stream) {
+  return decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, ws_bytes,
+                        (hipStream_t)stream);
 }
 
 extern "C" int mikv_decode_attention_finalize(const mikv_cache *c, int32_t length, const uint16_t *q,

@@ -8,11 +8,22 @@
 
 using namespace mikv;
 
+// Run the re-rank inside the finalize launch when the importance update is
+// fused and the cache has at most this many (sequence, KV head) pairs.
+// Fusing saves a launch but gives the finalize the select's larger resource
+// footprint (lower occupancy): measured on MI355X it helps 128 heads (GQA),
+// is neutral at 128-256 and costs 3 % at 1280.  0 turns fusing off.
+#ifndef MIKV_STEP_FUSE_SELECT_MAX_HEADS
+#define MIKV_STEP_FUSE_SELECT_MAX_HEADS 512
+#endif
+
+// Workspace of a step: the attention's, then the select's (256-byte aligned).
+static size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
 extern "C" size_t mikv_decode_step_workspace_size(const mikv_cache *c, int32_t length) {
   size_t a = mikv_decode_workspace_size(c, length);
   if (!a) return 0;
-  size_t s = mikv_select_workspace_size(c);
-  return ((a + 255) / 256) * 256 + s;
+  return align256(a) + mikv_select_workspace_size(c);
 }
 
 extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint16_t *q, const uint16_t *k_new,
@@ -32,7 +43,7 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
   const size_t need = mikv_decode_step_workspace_size(c, length);
   if (!workspace || workspace_bytes < need)
     return set_error(MIKV_ERR_CAPACITY, "mikv_decode_step: workspace too small (%zu < %zu)", workspace_bytes, need);
-  const size_t attn_ws = ((mikv_decode_workspace_size(c, length) + 255) / 256) * 256;
+  const size_t attn_ws = align256(mikv_decode_workspace_size(c, length));
   uint8_t *ws = (uint8_t *)workspace;
   hipStream_t st = (hipStream_t)stream;
   auto mark = [&](int i) {
@@ -42,10 +53,19 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
   rc = mikv_quantize_kv(c, k_new, v_new, balance, length - 1, 1, nullptr, nullptr, nullptr, 0, stream);
   if (rc) return rc;
   mark(1);
-  rc = mikv_decode_attention_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws,
-                                     stream);
+  rc = decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws, st);
   if (rc) return rc;
   mark(2);
+  if (fused && n_heads_of(c) <= MIKV_STEP_FUSE_SELECT_MAX_HEADS) {
+    // finalize, importance update and re-rank in one launch
+    rc = decode_finalize_select(c, length, q, balance, scale, out, probs_hi, probs_lo, ws, attn_ws, k_heavy, window,
+                                ws + attn_ws, st);
+    if (rc) return rc;
+    mark(3);
+    mark(4);
+    mark(5);
+    return MIKV_OK;
+  }
   rc = mikv_decode_attention_finalize(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws,
                                       stream);
   if (rc) return rc;
