@@ -262,6 +262,10 @@ def main():
         # per-launch algorithmic bytes / per-launch duration over the sampled
         # launches (each counts with its own step's bytes)
         achieved = sum(step_bytes[i] for i in sampled) / (sum(part_ms) * 1e-3) / 1e9
+        # An empty event bracket (the kernel-free "importance" phase of the
+        # fused step, measured in the diagnostic pass) shows the time the two
+        # events add to a bracketed launch.
+        overhead_ms = mean(dur["importance"]) if args.fused else float("nan")
         tr = measured_traffic(wl.name) if not args.override else None
         roofline = {"kernel": "attn_partial_kernel", "bound": "hbm", "achieved": round(achieved, 2),
                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
@@ -270,6 +274,7 @@ def main():
                                     "copy-calibrated)",
                     "mean_launch_us": round(mean(part_ms) * 1e3, 2),
                     "launches_timed": len(part_ms), "launch_timing": f"HIP events on every {every}-th timed step",
+                    "empty_event_bracket_us": round(overhead_ms * 1e3, 2) if overhead_ms == overhead_ms else None,
                     "algorithmic_bytes_per_launch": int(mean_bytes)}
         if tr:
             roofline["traffic_read_bytes"] = tr["read_bytes"]
