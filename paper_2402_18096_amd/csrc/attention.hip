@@ -230,10 +230,12 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   const uint32_t *vpb = Q ? (is_hi ? A.hi_vp : A.lo_vp) + (int64_t)h * cap * ng : nullptr;
   float *scores = is_hi ? A.scores_hi : A.scores_lo;
   const float s2scale = A.scale * kLog2e;
+  const float s2scale_q = Q ? __builtin_ldexpf(s2scale, 24) : s2scale;
 
   // Query (Eq. 4: q / balance), as fp16 pairs matching the format's pairing,
   // each pair pre-scaled by 2^-cls; with SPLITQ a second fp16 pair carries
-  // the rounding remainder.  qsum = sum of the lane's query channels (fp32).
+  // the rounding remainder.  qsum24 = 2^-24 * the sum of the lane's query
+  // channels (fp32).
   float m2[G], l[G], bsum[G], o[G][CPL];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
@@ -286,7 +288,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   // loads issued together, before any of them is used: the chunk's K/V
   // stream starts one memory round trip after the wave does.
   half2_t qh[G][NP], ql[G][SPLITQ ? NP : 1];
-  float qsum[G];
+  float qsum24[G];  // 2^-24 * sum of the lane's query channels
   uint4 qraw[G][CPL / 8];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
@@ -326,7 +328,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
     float s = 0.0f;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) s += qhat(c);
-    qsum[i] = s;
+    qsum24[i] = __builtin_ldexpf(s, -24);
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
       const float sc = __builtin_ldexpf(1.0f, -F::cls(p));
@@ -355,11 +357,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
       valid[u] = t < end;
       uint32_t kx[NP];
       F::template unpack<CPL>(cur[u].k, kx);
-      float ka = 1.0f, kbeta = 0.0f;
-      if constexpr (Q) {
-        ka = __builtin_ldexpf(f16_to_f32((uint16_t)(cur[u].kp & 0xffffu)), 24);
-        kbeta = f16_to_f32((uint16_t)(cur[u].kp >> 16));
-      }
+      const half2_t kab = as_h2(cur[u].kp);  // (alpha, beta) of the key group
 #pragma unroll
       for (int i = 0; i < G; ++i) {
         float d = 0.0f;
@@ -369,8 +367,11 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 #pragma unroll
           for (int p = 0; p < NP; ++p) d = __builtin_amdgcn_fdot2(as_h2(kx[p]), ql[i][p], d, false);
         }
-        float s = Q ? fmaf(ka, d, kbeta * qsum[i]) : d;
-        s = token_sum<LPT>(s) * s2scale;
+        // 2^-24 (alpha * 2^24 * d + beta * qsum): the fp16 scale and zero
+        // enter mixed-precision FMAs as stored; the power of two goes into
+        // the final scale, so the result is the same bits
+        float s = Q ? fmaf((float)kab.x, d, fmaf((float)kab.y, qsum24[i], 0.0f)) : d;
+        s = token_sum<LPT>(s) * s2scale_q;
         s = valid[u] ? s : kNegInf;
         s2[u][i] = s;
         if (scores && part == 0) s_lds[i * kMaxChunk + it * kPerIter + u * TPW + tsub] = s;
@@ -398,17 +399,15 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
     for (int u = 0; u < UNROLL; ++u) {
       uint32_t vx[NP];
       F::template unpack<CPL>(cur[u].v, vx);
-      float va = 1.0f, vbeta = 0.0f;
-      if constexpr (Q) {
-        va = f16_to_f32((uint16_t)(cur[u].vp & 0xffffu));
-        vbeta = f16_to_f32((uint16_t)(cur[u].vp >> 16));
-      }
+      const half2_t vab = as_h2(cur[u].vp);  // (alpha, beta) of the value group
 #pragma unroll
       for (int i = 0; i < G; ++i) {
-        const float e = valid[u] ? __builtin_amdgcn_exp2f(s2[u][i] - m2[i]) : 0.0f;
+        // past the pool s2 = -inf, and m2 is finite from the first iteration
+        // on (its first token is valid and raises the max), so e = 0
+        const float e = __builtin_amdgcn_exp2f(s2[u][i] - m2[i]);
         l[i] += e;
-        const float w = Q ? e * va : e;
-        if constexpr (Q) bsum[i] = fmaf(e, vbeta, bsum[i]);
+        const float w = Q ? fmaf(e, (float)vab.x, 0.0f) : e;
+        if constexpr (Q) bsum[i] = fmaf(e, (float)vab.y, bsum[i]);
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
           const half2_t hv = as_h2(vx[p]);
@@ -1023,15 +1022,21 @@ __device__ inline ProbTile<G> prob_tile_load(const AttnArgs &A, int h, int qh0, 
   return T;
 }
 
+// Probabilities of one tile, stored; with the importance update, the new
+// score of every slot also goes to a_new[u] (the old one past the pool).
 template <int G>
 __device__ inline void prob_tile_store(const AttnArgs &A, int h, int qh0, bool is_hi, bool accumulate,
-                                       const ProbTile<G> &T, const float M[G], const float inv[G]) {
+                                       const ProbTile<G> &T, const float M[G], const float inv[G],
+                                       float *a_new = nullptr) {
   const int cap = is_hi ? A.cap_hi : A.cap_lo;
   float *probs = is_hi ? A.probs_hi : A.probs_lo;
   float *acc = is_hi && accumulate ? A.acc : nullptr;
 #pragma unroll
   for (int u = 0; u < ProbTile<G>::kPer; ++u) {
-    if (T.t[u] >= T.n_pool) continue;
+    if (T.t[u] >= T.n_pool) {
+      if (a_new) a_new[u] = T.a[u];
+      continue;
+    }
     float sum = 0.0f;
 #pragma unroll
     for (int i = 0; i < G; ++i) {
@@ -1039,7 +1044,9 @@ __device__ inline void prob_tile_store(const AttnArgs &A, int h, int qh0, bool i
       if (probs) probs[(int64_t)(qh0 + i) * cap + T.t[u]] = p;
       sum = i == 0 ? p : sum + p;
     }
-    if (acc) acc[(int64_t)h * A.cap_hi + T.t[u]] = T.a[u] + sum;
+    const float an = T.a[u] + sum;
+    if (acc) acc[(int64_t)h * A.cap_hi + T.t[u]] = an;
+    if (a_new) a_new[u] = an;
   }
 }
 
@@ -1058,7 +1065,7 @@ __device__ inline void merge_output(const AttnArgs &A, int qh0, int nc, const fl
       invi = inv[j];
     }
   float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-#pragma unroll 4
+#pragma unroll 8
   for (int r = s; r < nc; r += S) {
     const float *rr = rec + (int64_t)r * kRec;
     const float mr = rr[0];
@@ -1085,16 +1092,20 @@ __device__ inline void merge_output(const AttnArgs &A, int qh0, int nc, const fl
   }
 }
 
+// Block (h, 0) merges the output of head h; blocks (h, 1..) turn one
+// probability tile each into probabilities (importance-pool tiles first).
+// Heads run along x, so the longest blocks, the merges, are dispatched first.
 template <int G>
 __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi,
                                                                int tiles_lo) {
-  const int h = blockIdx.y, c = blockIdx.x;
+  const int h = blockIdx.x, c = blockIdx.y;  // heads fastest: every head's block 0 is dispatched first
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
-  const bool is_hi = c < tiles_hi;
-  const bool has_tile = is_hi || c - tiles_hi < tiles_lo;
-  const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, is_hi, is_hi ? c : c - tiles_hi, has_tile, accumulate);
+  const int tile = c - 1;
+  const bool is_hi = tile < tiles_hi;
+  const bool has_tile = c > 0 && (is_hi || tile - tiles_hi < tiles_lo);
+  const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, is_hi, is_hi ? tile : tile - tiles_hi, has_tile, accumulate);
   float M[G], inv[G];
   head_stats<G>(A, qh0, nc, M, inv);
   if (c == 0) merge_output<G>(A, qh0, nc, M, inv);
@@ -1102,39 +1113,77 @@ __global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int a
 }
 
 // Finalize with the importance update and the re-rank fused (the decode
-// step): block 0 of head h merges the output, turns every importance-pool
-// tile into probabilities and score updates, and then, its own writes
-// being the only scores the re-rank reads, runs the head's top-k and
-// demotion; blocks 1.. handle the retained-pool tiles.  No block waits on
-// another.
+// step).  Block (h, 0) of head h turns every importance-pool tile into
+// probabilities and new scores and, its own writes being the only scores
+// the re-rank reads, runs the head's top-k and demotion on the scores it
+// still holds in registers (the positions and the last slot are loaded
+// with the tiles, so the re-rank adds one memory round trip: the demoted
+// row).  Block (h, 1) merges the output; blocks (h, 2..) handle the
+// retained-pool tiles.  Heads run along x, so every head's re-rank block is
+// dispatched before any tile block.  No block waits on another.
 template <int G, int HI, int LO>
 __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int tiles_hi, int tiles_lo, SelArgs S) {
-  const int h = blockIdx.y, c = blockIdx.x;
+  static_assert(kSel == kBlock && kSelItems * kBlock == 2 * kProbTile, "select items = two probability tiles");
+  const int h = blockIdx.x, c = blockIdx.y;  // heads fastest: every head's block 0 is dispatched first
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
   if (c > 0) {
-    const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, false, c - 1, c - 1 < tiles_lo, false);
+    const bool has_tile = c >= 2 && c - 2 < tiles_lo;
+    const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, false, c - 2, has_tile, false);
     float M[G], inv[G];
     head_stats<G>(A, qh0, nc, M, inv);
-    prob_tile_store<G>(A, h, qh0, false, false, T, M, inv);
+    if (c == 1)
+      merge_output<G>(A, qh0, nc, M, inv);
+    else if (has_tile)
+      prob_tile_store<G>(A, h, qh0, false, false, T, M, inv);
     return;
   }
-  // the first two importance-pool tiles are in flight with the statistics
-  // and the merge; larger pools continue tile by tile
+  // Everything the re-rank reads besides the new scores is loaded together
+  // with the first two tiles and the chunk statistics.
+  const int n = __builtin_amdgcn_readfirstlane(S.n_hi[h]);
+  const int n_lo0 = __builtin_amdgcn_readfirstlane(S.n_lo[h]);
+  const int thr = S.length - S.window;  // positions >= thr are in the window
+  // two tiles in flight for one or two query heads per KV head; with more,
+  // the second waits for the statistics (the block's register budget also
+  // bounds the occupancy of the retained-pool tile blocks)
+  constexpr bool kTwoAhead = G <= 2;
   const ProbTile<G> T0 = prob_tile_load<G>(A, h, qh0, true, 0, tiles_hi > 0, true);
-  const ProbTile<G> T1 = prob_tile_load<G>(A, h, qh0, true, 1, tiles_hi > 1, true);
+  ProbTile<G> T1;
+  if constexpr (kTwoAhead) T1 = prob_tile_load<G>(A, h, qh0, true, 1, tiles_hi > 1, true);
+  int pv[kSelItems];
+  const int32_t *pos = S.hi_pos + (int64_t)h * S.cap_hi;
+#pragma unroll
+  for (int u = 0; u < kSelItems; ++u) {
+    const int i = u * kSel + threadIdx.x;
+    pv[u] = i < S.cap_hi ? pos[i] : thr;
+  }
+  SlotData<HI> last = n > 0 ? load_slot<HI>(S, h, n - 1) : SlotData<HI>{};
   float M[G], inv[G];
   head_stats<G>(A, qh0, nc, M, inv);
-  merge_output<G>(A, qh0, nc, M, inv);
-  if (tiles_hi > 0) prob_tile_store<G>(A, h, qh0, true, true, T0, M, inv);
-  if (tiles_hi > 1) prob_tile_store<G>(A, h, qh0, true, true, T1, M, inv);
+  float an[kSelItems];
+  prob_tile_store<G>(A, h, qh0, true, true, T0, M, inv, an);
+  if constexpr (!kTwoAhead) T1 = prob_tile_load<G>(A, h, qh0, true, 1, tiles_hi > 1, true);
+  prob_tile_store<G>(A, h, qh0, true, true, T1, M, inv, an + ProbTile<G>::kPer);
   for (int tile = 2; tile < tiles_hi; ++tile) {
     const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, true, tile, true, true);
     prob_tile_store<G>(A, h, qh0, true, true, T, M, inv);
   }
-  __syncthreads();  // the block's score updates are complete before the re-rank reads them
-  select_head<HI, LO>(S, h);
+  // slot u * kSel + t of thread t is item u of the two first tiles
+  SelScan sc;
+  __shared__ float s_last;
+#pragma unroll
+  for (int u = 0; u < kSelItems; ++u) {
+    const int i = u * kSel + threadIdx.x;
+    if (i < n && pv[u] < thr) sc.add(i, pv[u], an[u]);
+    if (i == n - 1) s_last = an[u];
+  }
+  // slots past the first two tiles: from memory, written above by this same thread
+  if (S.cap_hi > kSel * kSelItems) select_scan(S, h, kSel * kSelItems, n, thr, sc);
+  __syncthreads();  // the block's score updates (and s_last) are complete before the re-rank uses them
+  if (threadIdx.x == 0 && n > 0)
+    last.acc = n - 1 < kSel * kSelItems ? s_last : S.hi_acc[(int64_t)h * S.cap_hi + n - 1];
+  select_finish<HI, LO>(S, h, n, n_lo0, sc, last);
 }
 
 template <int G>
@@ -1310,7 +1359,7 @@ int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int tiles_hi = (span_hi + kProbTile - 1) / kProbTile;  // probabilities accumulated
   const int tiles_lo = A.probs_lo ? (span_lo + kProbTile - 1) / kProbTile : 0;
-  dim3 grid(1 + tiles_lo, n_heads_of(c));  // block 0: output, importance pool, re-rank
+  dim3 grid(n_heads_of(c), 2 + tiles_lo);  // y = 0: importance pool and re-rank, 1: output
   const int G = group_size_of(c);
   switch (c->hi_bits * 100 + c->lo_bits) {
     case 1602: launch_finalize_select<16, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
@@ -1348,7 +1397,7 @@ extern "C" int mikv_decode_attention_finalize(const mikv_cache *c, int32_t lengt
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int tiles_hi = (A.scores_hi && (A.probs_hi || A.acc)) ? (span_hi + kProbTile - 1) / kProbTile : 0;
   const int tiles_lo = A.probs_lo ? (span_lo + kProbTile - 1) / kProbTile : 0;
-  dim3 grid(std::max(1, tiles_hi + tiles_lo), n_heads_of(c));
+  dim3 grid(n_heads_of(c), 1 + tiles_hi + tiles_lo);  // y = 0: output
   switch (group_size_of(c)) {
     case 1: hipLaunchKernelGGL(attn_finalize_kernel<1>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;
     case 2: hipLaunchKernelGGL(attn_finalize_kernel<2>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;

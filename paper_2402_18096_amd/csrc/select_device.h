@@ -280,26 +280,28 @@ __device__ inline void store_slot(const SelArgs &A, int h, int dst, const SlotDa
 
 constexpr int kSelItems = 16;  // importance-pool slots per thread held in registers
 
-// Re-rank and demote for head h; the whole block (kSel threads) takes part.
-template <int HI_BITS, int LO_BITS>
-__device__ void select_head(const SelArgs &A, int h) {
-  __shared__ int s_tmp_i[kSel / 64];
-  __shared__ uint64_t s_tmp_u[kSel / 64];
-  __shared__ int s_arg[3];
-  const int n = __builtin_amdgcn_readfirstlane(A.n_hi[h]);
-  const int n_lo0 = __builtin_amdgcn_readfirstlane(A.n_lo[h]);
-  const int thr = A.length - A.window;  // positions >= thr are in the window
-  const int32_t *pos = A.hi_pos + (int64_t)h * A.cap_hi;
-  const float *acc = A.hi_acc + (int64_t)h * A.cap_hi;
-  auto elig = [&](int i) { return pos[i] < thr; };
-  auto key = [&](int i) { return rank_key(acc[i], pos[i]); };
-
-  // One pass over the pool, kSel * kSelItems slots per round trip: count
-  // the eligible slots and keep the least important one.  The loads run to
-  // the capacity, so they need not wait for the pool count.
+// The running candidate state of one thread: eligible slots seen and the
+// least important of them (key and slot).
+struct SelScan {
   int cnt = 0, arg = -1;
   uint64_t mn = ~0ull;
-  for (int base = 0; base < A.cap_hi; base += kSel * kSelItems) {
+  __device__ inline void add(int slot, int p, float score) {
+    ++cnt;
+    const uint64_t k = rank_key(score, p);
+    if (k < mn) {
+      mn = k;
+      arg = slot;
+    }
+  }
+};
+
+// Scan slots [from, cap_hi) of head h from memory, kSel * kSelItems slots
+// per round trip; thread t reads slots t, t + kSel, ...  The loads run to
+// the capacity, so they need not wait for the pool count.
+__device__ inline void select_scan(const SelArgs &A, int h, int from, int n, int thr, SelScan &sc) {
+  const int32_t *pos = A.hi_pos + (int64_t)h * A.cap_hi;
+  const float *acc = A.hi_acc + (int64_t)h * A.cap_hi;
+  for (int base = from; base < A.cap_hi; base += kSel * kSelItems) {
     int pv[kSelItems];
     float av[kSelItems];
 #pragma unroll
@@ -310,20 +312,28 @@ __device__ void select_head(const SelArgs &A, int h) {
     }
 #pragma unroll
     for (int u = 0; u < kSelItems; ++u) {
-      if (base + u * kSel + (int)threadIdx.x < n && pv[u] < thr) {
-        ++cnt;
-        const uint64_t k = rank_key(av[u], pv[u]);
-        if (k < mn) {
-          mn = k;
-          arg = base + u * kSel + threadIdx.x;
-        }
-      }
+      const int i = base + u * kSel + threadIdx.x;
+      if (i < n && pv[u] < thr) sc.add(i, pv[u], av[u]);
     }
   }
-  // The last slot fills the hole of a demoted token: fetch it now, its
-  // latency then hides behind the reductions.
-  const SlotData<HI_BITS> last = n > 0 ? load_slot<HI_BITS>(A, h, n - 1) : SlotData<HI_BITS>{};
-  const int n_elig = block_sum_int(cnt, s_tmp_i);
+}
+
+// Second half of the re-rank of head h, once every thread has scanned its
+// slots: count, find the cut, demote and refill.  `n` and `n_lo0` are the
+// pool counts before the re-rank, `last` the prefetched last slot.
+template <int HI_BITS, int LO_BITS>
+__device__ void select_finish(const SelArgs &A, int h, int n, int n_lo0, const SelScan &sc,
+                              const SlotData<HI_BITS> &last) {
+  __shared__ int s_tmp_i[kSel / 64];
+  __shared__ uint64_t s_tmp_u[kSel / 64];
+  __shared__ int s_arg[3];
+  const int thr = A.length - A.window;  // positions >= thr are in the window
+  const int32_t *pos = A.hi_pos + (int64_t)h * A.cap_hi;
+  const float *acc = A.hi_acc + (int64_t)h * A.cap_hi;
+  auto elig = [&](int i) { return pos[i] < thr; };
+  auto key = [&](int i) { return rank_key(acc[i], pos[i]); };
+
+  const int n_elig = block_sum_int(sc.cnt, s_tmp_i);
   const int n_dem = n_elig - A.k_heavy;
   if (n_dem <= 0) return;
   if (n_lo0 + n_dem > A.cap_lo) {
@@ -334,8 +344,8 @@ __device__ void select_head(const SelArgs &A, int h) {
   if (n_dem == 1) {
     // Steady state of decoding: the least important eligible token leaves;
     // the last slot fills its hole.
-    const uint64_t cut = block_min_u64(mn, s_tmp_u);
-    if (arg >= 0 && mn == cut) s_arg[0] = arg;
+    const uint64_t cut = block_min_u64(sc.mn, s_tmp_u);
+    if (sc.arg >= 0 && sc.mn == cut) s_arg[0] = sc.arg;
     __syncthreads();
     const int slot = s_arg[0];
     // the key's low word is the position
@@ -408,6 +418,19 @@ __device__ void select_head(const SelArgs &A, int h) {
     A.n_hi[h] = n_new;
     A.n_lo[h] = n_lo0 + n_dem;
   }
+}
+
+// Re-rank and demote for head h; the whole block (kSel threads) takes part.
+template <int HI_BITS, int LO_BITS>
+__device__ void select_head(const SelArgs &A, int h) {
+  const int n = __builtin_amdgcn_readfirstlane(A.n_hi[h]);
+  const int n_lo0 = __builtin_amdgcn_readfirstlane(A.n_lo[h]);
+  SelScan sc;
+  select_scan(A, h, 0, n, A.length - A.window, sc);
+  // The last slot fills the hole of a demoted token: fetch it now, its
+  // latency then hides behind the reductions.
+  const SlotData<HI_BITS> last = n > 0 ? load_slot<HI_BITS>(A, h, n - 1) : SlotData<HI_BITS>{};
+  select_finish<HI_BITS, LO_BITS>(A, h, n, n_lo0, sc, last);
 }
 
 // Arguments of a select for the cache `c` (host side).
