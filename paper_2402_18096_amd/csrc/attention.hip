@@ -34,6 +34,7 @@
 // probabilities and optionally adds them to the importance scores.
 #include <algorithm>
 
+#include "append_device.h"
 #include "mikv_internal.h"
 #include "select_device.h"
 
@@ -71,7 +72,17 @@ struct AttnArgs {
   float *out;                    // [B*Hq, 128]
   int cap_hi, cap_lo, group, q_heads, kv_heads;
   int chunk_hi, chunk_lo, nc_hi, nc_lo;
+  // Decode step: the new token is appended by the partial phase (app.k
+  // non-NULL) and n_hi does not count it until the re-rank writes it.
+  AppendArgs app;
+  int hi_pending;
 };
+
+// Importance-pool tokens of head h, the pending new token included.
+__device__ inline int hi_count(const AttnArgs &A, int h) {
+  const int n = A.n_hi[h];
+  return n + (A.hi_pending && n < A.cap_hi ? 1 : 0);
+}
 
 // ---------------------------------------------------------------------------
 // Packed-row formats.  A lane's CPL channels are held as NP = CPL/2 fp16
@@ -219,7 +230,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   // wave-uniform, so the buffer descriptors built from it live in scalar
   // registers (a value the compiler thinks divergent would wrap every load in
   // a per-lane loop).
-  const int n_pool = __builtin_amdgcn_readfirstlane(is_hi ? A.n_hi[h] : A.n_lo[h]);
+  const int n_pool = __builtin_amdgcn_readfirstlane(is_hi ? hi_count(A, h) : A.n_lo[h]);
   const int start = chunk * chunk_len;
   const int end = min(start + chunk_len, n_pool);
   constexpr int64_t kRow = BITS == 16 ? kHeadDim * 2 : kHeadDim * BITS / 8;
@@ -930,6 +941,27 @@ constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PR
 #define MIKV_CHUNK_KB 96
 #endif
 
+// The decode step's new token: written into importance-pool slot n_hi by
+// the wave whose chunk holds that slot, before the wave reads its chunk (no
+// other wave reads the slot, and chunks are whole iterations, so no other
+// wave's loads reach it).  A full pool sets the status bit instead (wave
+// of chunk 0).
+template <int HI>
+__device__ inline void append_in_chunk(const AttnArgs &A, int h, int chunk) {
+  const int n0 = __builtin_amdgcn_readfirstlane(A.n_hi[h]);
+  const int lane = threadIdx.x & 63;
+  if (n0 >= A.cap_hi) {
+    if (chunk == 0 && lane == 0) atomicOr(A.app.status, MIKV_DEVERR_HI_FULL);
+    return;
+  }
+  if (chunk != n0 / A.chunk_hi) return;
+  if (lane < 8) append_row<HI>(A.app, h, n0, lane);
+  // the lanes that read the slot see the stored row (one wave per block)
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 template <int HI, int LO, int G, bool SPLITQ>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
@@ -937,6 +969,7 @@ void attn_partial_kernel(AttnArgs A) {
   const int h = blockIdx.y, c = blockIdx.x;
   __shared__ float s_lds[G * kMaxChunk];  // the chunk's scores, [G][kMaxChunk]
   if (c < A.nc_hi) {
+    if (A.hi_pending) append_in_chunk<HI>(A, h, c);
     attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
   } else if constexpr (LO == 2 && G >= 2) {
     __shared__ __align__(16) _Float16 w_lds[kWLds];  // value-MFMA weights, see w_index
@@ -1018,7 +1051,7 @@ __device__ inline ProbTile<G> prob_tile_load(const AttnArgs &A, int h, int qh0, 
     for (int i = 0; i < G; ++i) T.sv[u][i] = ok ? scores[(int64_t)(qh0 + i) * cap + T.t[u]] : 0.0f;
     T.a[u] = ok && acc ? acc[(int64_t)h * A.cap_hi + T.t[u]] : 0.0f;
   }
-  T.n_pool = has_tile ? (is_hi ? A.n_hi[h] : A.n_lo[h]) : 0;
+  T.n_pool = has_tile ? (is_hi ? hi_count(A, h) : A.n_lo[h]) : 0;
   return T;
 }
 
@@ -1095,9 +1128,11 @@ __device__ inline void merge_output(const AttnArgs &A, int qh0, int nc, const fl
 // Block (h, 0) merges the output of head h; blocks (h, 1..) turn one
 // probability tile each into probabilities (importance-pool tiles first).
 // Heads run along x, so the longest blocks, the merges, are dispatched first.
+// (Register budget: 8 blocks per CU for one query head per KV head, 6 for
+// two; the grids of many-head caches hold several blocks per CU.)
 template <int G>
-__global__ __launch_bounds__(kBlock) void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi,
-                                                               int tiles_lo) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(G == 1 ? 8 : G == 2 ? 6 : 1)))
+void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi, int tiles_lo) {
   const int h = blockIdx.x, c = blockIdx.y;  // heads fastest: every head's block 0 is dispatched first
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
@@ -1141,7 +1176,7 @@ __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int
   }
   // Everything the re-rank reads besides the new scores is loaded together
   // with the first two tiles and the chunk statistics.
-  const int n = __builtin_amdgcn_readfirstlane(S.n_hi[h]);
+  const int n = __builtin_amdgcn_readfirstlane(hi_count(A, h));
   const int n_lo0 = __builtin_amdgcn_readfirstlane(S.n_lo[h]);
   const int thr = S.length - S.window;  // positions >= thr are in the window
   // two tiles in flight for one or two query heads per KV head; with more,
@@ -1183,7 +1218,7 @@ __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int
   __syncthreads();  // the block's score updates (and s_last) are complete before the re-rank uses them
   if (threadIdx.x == 0 && n > 0)
     last.acc = n - 1 < kSel * kSelItems ? s_last : S.hi_acc[(int64_t)h * S.cap_hi + n - 1];
-  select_finish<HI, LO>(S, h, n, n_lo0, sc, last);
+  select_finish<HI, LO>(S, h, n, n_lo0, sc, last, A.hi_pending != 0);
 }
 
 template <int G>
@@ -1266,7 +1301,33 @@ AttnArgs make_args(const mikv_cache *c, const Plan &p, const uint16_t *q, const 
   A.chunk_lo = p.chunk_lo;
   A.nc_hi = p.nc_hi;
   A.nc_lo = p.nc_lo;
+  A.app = AppendArgs{};
+  A.hi_pending = 0;
   return A;
+}
+
+// The fold of the decode step's append into the attention (position
+// length - 1).
+void set_append(AttnArgs &A, const mikv_cache *c, int32_t length, const uint16_t *k_new, const uint16_t *v_new,
+                const float *balance) {
+  AppendArgs &a = A.app;
+  a.hi_k = (uint8_t *)c->hi_k;
+  a.hi_v = (uint8_t *)c->hi_v;
+  a.hi_kp = (uint32_t *)c->hi_kp;
+  a.hi_vp = (uint32_t *)c->hi_vp;
+  a.hi_pos = c->hi_pos;
+  a.hi_acc = c->hi_acc;
+  a.map = c->map;
+  a.status = c->status;
+  a.k = k_new;
+  a.v = v_new;
+  a.balance = balance;
+  a.score_init = nullptr;
+  a.cap_hi = c->cap_hi;
+  a.max_len = c->max_len;
+  a.group = c->group;
+  a.pos = length - 1;
+  A.hi_pending = 1;
 }
 
 template <int HI, int LO, bool SPLITQ>
@@ -1319,11 +1380,12 @@ namespace mikv {
 
 int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
                    float *out, float *probs_hi, float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
-                   hipStream_t st) {
+                   const uint16_t *k_new, const uint16_t *v_new, hipStream_t st) {
   int rc = check_attention_args(c, length, q, balance, out, ws, ws_bytes, "mikv_decode_attention_partial");
   if (rc) return rc;
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, flags, ws);
+  if (k_new) set_append(A, c, length, k_new, v_new, balance);
   dim3 grid(p.nc_hi + p.nc_lo, n_heads_of(c));
   const int G = group_size_of(c);
   switch (c->hi_bits * 100 + c->lo_bits) {
@@ -1350,11 +1412,12 @@ void launch_finalize_select(const AttnArgs &A, const SelArgs &S, int G, dim3 gri
 
 int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
                            float *out, float *probs_hi, float *probs_lo, void *ws, size_t ws_bytes, int32_t k_heavy,
-                           int32_t window, void *sel_ws, hipStream_t st) {
+                           int32_t window, void *sel_ws, bool appended, hipStream_t st) {
   int rc = check_attention_args(c, length, q, balance, out, ws, ws_bytes, "mikv_decode_step");
   if (rc) return rc;
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, MIKV_ATTN_ACCUMULATE, ws);
+  A.hi_pending = appended ? 1 : 0;
   const SelArgs S = make_sel_args(c, length, k_heavy, window, sel_ws);
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int tiles_hi = (span_hi + kProbTile - 1) / kProbTile;  // probabilities accumulated
@@ -1378,7 +1441,7 @@ extern "C" int mikv_decode_attention_partial(const mikv_cache *c, int32_t length
                                              const float *balance, float scale, float *out, float *probs_hi,
                                              float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
                                              void *stream) {
-  return decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, ws_bytes,
+  return decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, ws_bytes, nullptr, nullptr,
                         (hipStream_t)stream);
 }
 

@@ -24,15 +24,17 @@ int check_launch(const char *what);
 int validate_cache(const mikv_cache *c);
 
 // Internal launches of the decode step (attention.hip): the attention's
-// partial phase; and the finalize with the importance update and the
-// re-rank fused (block 0 of each head updates the head's scores, then runs
-// its select).
+// partial phase, which with k_new/v_new non-NULL also appends the new token
+// (position length - 1) to the importance pool, leaving n_hi to the
+// finalize; and the finalize with the importance update and the re-rank
+// fused (block 0 of each head updates the head's scores, then runs its
+// select), which with `appended` set counts that token into n_hi.
 int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
                    float *out, float *probs_hi, float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
-                   hipStream_t st);
+                   const uint16_t *k_new, const uint16_t *v_new, hipStream_t st);
 int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
                            float *out, float *probs_hi, float *probs_lo, void *ws, size_t ws_bytes, int32_t k_heavy,
-                           int32_t window, void *sel_ws, hipStream_t st);
+                           int32_t window, void *sel_ws, bool appended, hipStream_t st);
 
 inline int group_size_of(const mikv_cache *c) { return c->q_heads / c->kv_heads; }
 inline int n_heads_of(const mikv_cache *c) { return c->batch * c->kv_heads; }

@@ -6,6 +6,7 @@
 // quantization group of g channels spans g/32 adjacent lanes, which combine
 // their min/max with lane shuffles.  Loads are 4 x 16 B per lane, contiguous
 // across the lanes of a row (coalesced); codes are written as whole dwords.
+#include "append_device.h"
 #include "mikv_internal.h"
 
 namespace mikv {
@@ -13,65 +14,6 @@ namespace mikv {
 namespace {
 
 constexpr int kChunk = 256;  // tokens per block in the placement kernels
-
-// Load 32 fp16 channels starting at `src` (16-byte aligned) into fp32,
-// multiplied by the balancer when one is given (Eq. 3; one fp32 product).
-__device__ inline void load_row_segment(const uint16_t *src, const float *bal, float x[32]) {
-  const uint4 *s4 = reinterpret_cast<const uint4 *>(src);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    uint4 w = s4[i];
-    uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      x[i * 8 + 2 * j] = f16_to_f32((uint16_t)(ws[j] & 0xffffu));
-      x[i * 8 + 2 * j + 1] = f16_to_f32((uint16_t)(ws[j] >> 16));
-    }
-  }
-  if (bal) {
-#pragma unroll
-    for (int c = 0; c < 32; ++c) x[c] = x[c] * bal[c];
-  }
-}
-
-// Eq. 1 codes of one 32-channel segment at BITS: group min/max (a group of
-// g channels spans g/32 adjacent lanes, combined with shuffles), the group's
-// fp16 (alpha, beta) and the packed little-endian words w[BITS].
-template <int BITS>
-__device__ inline GroupParams quantize_words(const float x[32], int group, uint32_t w[BITS]) {
-  float mn = x[0], mx = x[0];
-#pragma unroll
-  for (int c = 1; c < 32; ++c) {
-    mn = fminf(mn, x[c]);
-    mx = fmaxf(mx, x[c]);
-  }
-  // combine across the lanes of one group (group/32 lanes, aligned)
-  for (int o = 1; o < group / 32; o <<= 1) {
-    mn = fminf(mn, __shfl_xor(mn, o, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-  }
-  GroupParams p = group_params(mn, mx, BITS);
-#pragma unroll
-  for (int i = 0; i < BITS; ++i) w[i] = 0u;
-#pragma unroll
-  for (int c = 0; c < 32; ++c) w[(c * BITS) / 32] |= encode(x[c], p, BITS) << ((c * BITS) % 32);
-  return p;
-}
-
-// Quantize one 32-channel segment (lane part `lane4` of its row) at BITS:
-// writes the packed codes (32*BITS/8 bytes at `codes`) and, from the first
-// lane of each group, the (alpha, beta) pair at `param`.
-template <int BITS>
-__device__ inline void quantize_segment(const float x[32], int group, int lane4, uint8_t *codes,
-                                        uint32_t *param, bool store) {
-  uint32_t w[BITS];
-  GroupParams p = quantize_words<BITS>(x, group, w);
-  if (!store) return;
-  uint32_t *dst = reinterpret_cast<uint32_t *>(codes);
-#pragma unroll
-  for (int i = 0; i < BITS; ++i) dst[i] = w[i];
-  if ((lane4 % (group / 32)) == 0) *param = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
-}
 
 template <int BITS>
 __global__ __launch_bounds__(256) void quantize_rows_kernel(const uint16_t *x, int64_t rows,
@@ -130,6 +72,28 @@ Pools make_pools(const mikv_cache *c) {
   p.group = c->group;
   p.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
   return p;
+}
+
+__host__ __device__ inline AppendArgs append_args(const Pools &P, const uint16_t *k, const uint16_t *v,
+                                                  const float *balance, int pos, const float *score_init) {
+  AppendArgs a;
+  a.hi_k = P.hi_k;
+  a.hi_v = P.hi_v;
+  a.hi_kp = P.hi_kp;
+  a.hi_vp = P.hi_vp;
+  a.hi_pos = P.hi_pos;
+  a.hi_acc = P.hi_acc;
+  a.map = P.map;
+  a.status = P.status;
+  a.k = k;
+  a.v = v;
+  a.balance = balance;
+  a.score_init = score_init;
+  a.cap_hi = P.cap_hi;
+  a.max_len = P.max_len;
+  a.group = P.group;
+  a.pos = pos;
+  return a;
 }
 
 // Count importance tokens per chunk of kChunk tokens: counts[h, chunk].
@@ -290,9 +254,8 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
 }
 
 // One new token per head into the importance pool (the decoding step):
-// 8 lanes per head, lanes 0-3 the key row, 4-7 the value row.  The slot
-// count and the rows are loaded together; lane 0 of the head records the
-// position, the initial score and the map entry, and advances n_hi.
+// 8 lanes per head, lanes 0-3 the key row, 4-7 the value row; lane 0 of the
+// head then advances n_hi (or flags a full pool).
 template <int HI_BITS>
 __global__ __launch_bounds__(64) void append_one_kernel(Pools P, const uint16_t *k, const uint16_t *v,
                                                         const float *balance, int pos, const float *score_init,
@@ -300,38 +263,13 @@ __global__ __launch_bounds__(64) void append_one_kernel(Pools P, const uint16_t 
   const int t = blockIdx.x * 64 + threadIdx.x;
   const int h = t >> 3;
   if (h >= n_heads) return;  // all 8 lanes of a head leave together
-  const int is_v = (t >> 2) & 1, lane4 = t & 3;
   const int n0 = P.n_hi[h];
-  const float *bal = (!is_v && balance) ? balance + (int64_t)h * kHeadDim + lane4 * 32 : nullptr;
-  float x[32];
-  load_row_segment((is_v ? v : k) + (int64_t)h * kHeadDim + lane4 * 32, bal, x);
-  const bool store = n0 < P.cap_hi;
-  const int64_t slot = (int64_t)h * P.cap_hi + (store ? n0 : 0);
-  if (HI_BITS == 16) {
-    if (store) {
-      uint32_t w[16];
-#pragma unroll
-      for (int c = 0; c < 16; ++c)
-        w[c] = pack_f16x2(x[2 * c], x[2 * c + 1]);
-      uint4 *d4 = reinterpret_cast<uint4 *>((is_v ? P.hi_v : P.hi_k) + (slot * kHeadDim + lane4 * 32) * 2);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) d4[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
-    }
-  } else {
-    const int ng = kHeadDim / P.group;
-    uint8_t *dst = (is_v ? P.hi_v : P.hi_k) + slot * kHeadDim + lane4 * 32;
-    uint32_t *par = (is_v ? P.hi_vp : P.hi_kp) + slot * ng + (lane4 * 32) / P.group;
-    quantize_segment<8>(x, P.group, lane4, dst, par, store);
-  }
-  if ((t & 7) == 0) {
-    if (store) {
-      P.hi_pos[slot] = pos;
-      P.hi_acc[slot] = score_init ? score_init[h] : 0.0f;
-      if (P.map) P.map[(int64_t)h * P.max_len + pos] = 1;
-      P.n_hi[h] = n0 + 1;
-    } else {
-      atomicOr(P.status, MIKV_DEVERR_HI_FULL);
-    }
+  if (n0 < P.cap_hi) {  // the same for the 8 lanes of the head
+    const AppendArgs app = append_args(P, k, v, balance, pos, score_init);
+    append_row<HI_BITS>(app, h, n0, t & 7);
+    if ((t & 7) == 0) P.n_hi[h] = n0 + 1;
+  } else if ((t & 7) == 0) {
+    atomicOr(P.status, MIKV_DEVERR_HI_FULL);
   }
 }
 

@@ -320,10 +320,12 @@ __device__ inline void select_scan(const SelArgs &A, int h, int from, int n, int
 
 // Second half of the re-rank of head h, once every thread has scanned its
 // slots: count, find the cut, demote and refill.  `n` and `n_lo0` are the
-// pool counts before the re-rank, `last` the prefetched last slot.
+// pool counts before the re-rank, `last` the prefetched last slot.  With
+// `set_n` (n_hi in memory does not yet count an appended token) n_hi is
+// written even when no token leaves.
 template <int HI_BITS, int LO_BITS>
 __device__ void select_finish(const SelArgs &A, int h, int n, int n_lo0, const SelScan &sc,
-                              const SlotData<HI_BITS> &last) {
+                              const SlotData<HI_BITS> &last, bool set_n = false) {
   __shared__ int s_tmp_i[kSel / 64];
   __shared__ uint64_t s_tmp_u[kSel / 64];
   __shared__ int s_arg[3];
@@ -335,9 +337,11 @@ __device__ void select_finish(const SelArgs &A, int h, int n, int n_lo0, const S
 
   const int n_elig = block_sum_int(sc.cnt, s_tmp_i);
   const int n_dem = n_elig - A.k_heavy;
-  if (n_dem <= 0) return;
-  if (n_lo0 + n_dem > A.cap_lo) {
-    if (threadIdx.x == 0) atomicOr(A.status, MIKV_DEVERR_LO_FULL);
+  if (n_dem <= 0 || n_lo0 + n_dem > A.cap_lo) {
+    if (threadIdx.x == 0) {
+      if (n_dem > 0) atomicOr(A.status, MIKV_DEVERR_LO_FULL);
+      if (set_n) A.n_hi[h] = n;
+    }
     return;
   }
 

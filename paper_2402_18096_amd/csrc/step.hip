@@ -50,22 +50,28 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
     if (phase_events && phase_events[i]) hipEventRecord((hipEvent_t)phase_events[i], st);
   };
   mark(0);
-  rc = mikv_quantize_kv(c, k_new, v_new, balance, length - 1, 1, nullptr, nullptr, nullptr, 0, stream);
-  if (rc) return rc;
-  mark(1);
-  rc = decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws, st);
-  if (rc) return rc;
-  mark(2);
   if (fused && n_heads_of(c) <= MIKV_STEP_FUSE_SELECT_MAX_HEADS) {
-    // finalize, importance update and re-rank in one launch
+    // Two launches: the attention's partial phase, which also appends the
+    // new token; then finalize, importance update and re-rank.
+    mark(1);
+    rc = decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws, k_new, v_new, st);
+    if (rc) return rc;
+    mark(2);
     rc = decode_finalize_select(c, length, q, balance, scale, out, probs_hi, probs_lo, ws, attn_ws, k_heavy, window,
-                                ws + attn_ws, st);
+                                ws + attn_ws, true, st);
     if (rc) return rc;
     mark(3);
     mark(4);
     mark(5);
     return MIKV_OK;
   }
+  rc = mikv_quantize_kv(c, k_new, v_new, balance, length - 1, 1, nullptr, nullptr, nullptr, 0, stream);
+  if (rc) return rc;
+  mark(1);
+  rc = decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws, nullptr, nullptr,
+                      st);
+  if (rc) return rc;
+  mark(2);
   rc = mikv_decode_attention_finalize(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws,
                                       stream);
   if (rc) return rc;
