@@ -33,6 +33,7 @@
 // scores; the finalize phase merges the records exactly, turns scores into
 // probabilities and optionally adds them to the importance scores.
 #include <algorithm>
+#include <type_traits>
 
 #include "append_device.h"
 #include "mikv_internal.h"
@@ -71,7 +72,7 @@ struct AttnArgs {
   float *acc;                    // hi_acc when accumulating (nullable)
   float *out;                    // [B*Hq, 128]
   int cap_hi, cap_lo, group, q_heads, kv_heads;
-  int chunk_hi, chunk_lo, nc_hi, nc_lo;
+  int chunk_hi, chunk_lo, nc_hi, nc_lo, nc_first;
   // Decode step: the new token is appended by the partial phase (app.k
   // non-NULL) and n_hi does not count it until the re-rank writes it.
   AppendArgs app;
@@ -184,33 +185,42 @@ __device__ inline rsrc_t make_rsrc(const void *base, uint32_t bytes) {
 
 // Load one token's row segments (this lane's channels) and group params at
 // byte offsets `orow` (rows) and `opar` (params) of the head's pools.
-template <int BITS, int CPL>
+// WHICH: 1 the key segment and its group parameters, 2 the value's, 3 both.
+template <int BITS, int CPL, int WHICH = 3>
 __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, rsrc_t rkp, rsrc_t rvp, uint32_t orow,
                                      uint32_t opar) {
   constexpr int KW = Rows<BITS, CPL>::KW;
+  constexpr bool LK = (WHICH & 1) != 0, LV = (WHICH & 2) != 0;
   if constexpr (KW >= 4) {
 #pragma unroll
     for (int i = 0; i < KW / 4; ++i) {
-      auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, orow + 16 * i, 0, 0);
-      auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, orow + 16 * i, 0, 0);
+      if constexpr (LK) {
+        auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, orow + 16 * i, 0, 0);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        r.k[4 * i + j] = a[j];
-        r.v[4 * i + j] = b[j];
+        for (int j = 0; j < 4; ++j) r.k[4 * i + j] = a[j];
+      }
+      if constexpr (LV) {
+        auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, orow + 16 * i, 0, 0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) r.v[4 * i + j] = b[j];
       }
     }
   } else if constexpr (KW == 2) {
-    auto a = __builtin_amdgcn_raw_buffer_load_b64(rk, orow, 0, 0);
-    auto b = __builtin_amdgcn_raw_buffer_load_b64(rv, orow, 0, 0);
-    r.k[0] = a[0]; r.k[1] = a[1];
-    r.v[0] = b[0]; r.v[1] = b[1];
+    if constexpr (LK) {
+      auto a = __builtin_amdgcn_raw_buffer_load_b64(rk, orow, 0, 0);
+      r.k[0] = a[0]; r.k[1] = a[1];
+    }
+    if constexpr (LV) {
+      auto b = __builtin_amdgcn_raw_buffer_load_b64(rv, orow, 0, 0);
+      r.v[0] = b[0]; r.v[1] = b[1];
+    }
   } else {
-    r.k[0] = __builtin_amdgcn_raw_buffer_load_b32(rk, orow, 0, 0);
-    r.v[0] = __builtin_amdgcn_raw_buffer_load_b32(rv, orow, 0, 0);
+    if constexpr (LK) r.k[0] = __builtin_amdgcn_raw_buffer_load_b32(rk, orow, 0, 0);
+    if constexpr (LV) r.v[0] = __builtin_amdgcn_raw_buffer_load_b32(rv, orow, 0, 0);
   }
   if constexpr (BITS != 16) {
-    r.kp = __builtin_amdgcn_raw_buffer_load_b32(rkp, opar, 0, 0);
-    r.vp = __builtin_amdgcn_raw_buffer_load_b32(rvp, opar, 0, 0);
+    if constexpr (LK) r.kp = __builtin_amdgcn_raw_buffer_load_b32(rkp, opar, 0, 0);
+    if constexpr (LV) r.vp = __builtin_amdgcn_raw_buffer_load_b32(rvp, opar, 0, 0);
   }
 }
 
@@ -264,7 +274,6 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   constexpr int kSeg = Rows<BITS, CPL>::KW * 4;  // bytes of one lane's row segment
   const int n_iter = end > start ? (end - start + kPerIter - 1) / kPerIter : 0;
   const int first = start + wave * TPW * UNROLL + tsub;  // this lane's token in iteration 0, u = 0
-  auto tok_of = [&](int it, int u) { return first + it * kPerIter + u * TPW; };
   const int g_lane = (part * CPL) / A.group;
   // Buffer resources over this head's occupied slots; a lane's offset is
   // fixed per iteration and the unroll steps are immediate offsets.
@@ -276,14 +285,20 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   const uint32_t off_row0 = lane_tok * (uint32_t)kRow + (uint32_t)(part * kSeg);
   const uint32_t off_par0 = (lane_tok * (uint32_t)ng + (uint32_t)g_lane) * 4u;
 
-  auto load_it = [&](Rows<BITS, CPL>(&r)[UNROLL], int it) {
+  // With `live` false the loads go through empty descriptors: they return
+  // zero without a memory access, so a load needs no branch around it.
+  const rsrc_t r_none = make_rsrc(kb, 0u);
+  auto load_part = [&](auto which, Rows<BITS, CPL>(&r)[UNROLL], int it, bool live = true) {
     const uint32_t orow = off_row0 + (uint32_t)(it * kPerIter) * (uint32_t)kRow;
     const uint32_t opar = off_par0 + (uint32_t)(it * kPerIter) * (uint32_t)ng * 4u;
+    const rsrc_t ak = live ? rk : r_none, av = live ? rv : r_none;
+    const rsrc_t akp = live ? rkp : r_none, avp = live ? rvp : r_none;
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
-      load_seg_rows<BITS, CPL>(r[u], rk, rv, rkp, rvp, orow + (uint32_t)(u * TPW * kRow),
-                               opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u);
+      load_seg_rows<BITS, CPL, decltype(which)::value>(r[u], ak, av, akp, avp, orow + (uint32_t)(u * TPW * kRow),
+                                                       opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u);
   };
+  auto load_it = [&](Rows<BITS, CPL>(&r)[UNROLL], int it) { load_part(std::integral_constant<int, 3>{}, r, it); };
 
   // The first iterations' rows do not depend on the query: issue them first.
   Rows<BITS, CPL> cur[UNROLL], n1[PREFETCH >= 1 ? UNROLL : 1], n2[PREFETCH >= 2 ? UNROLL : 1];
@@ -358,14 +373,15 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 #pragma unroll
   for (int i = 0; i < G; ++i) score_row[i] = scores ? scores + (int64_t)(qh0 + i) * cap : nullptr;
 
-  auto proc = [&](Rows<BITS, CPL>(&cur)[UNROLL], int it) {
-    float s2[UNROLL][G];
+  float s2[UNROLL][G];
+  // Scores of one iteration (and the lazy running-max update).
+  auto proc_k = [&](Rows<BITS, CPL>(&cur)[UNROLL], int it) {
     bool valid[UNROLL];
-    bool raise = false;
+    uint64_t raise = 0;  // lanes whose score passes the lazy threshold (a ballot per token)
+    const int rem = end - it * kPerIter;  // wave-uniform: a token is valid when first + u * TPW < rem
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      const int t = tok_of(it, u);
-      valid[u] = t < end;
+      valid[u] = first < rem - u * TPW;
       uint32_t kx[NP];
       F::template unpack<CPL>(cur[u].k, kx);
       const half2_t kab = as_h2(cur[u].kp);  // (alpha, beta) of the key group
@@ -385,11 +401,14 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
         s = token_sum<LPT>(s) * s2scale_q;
         s = valid[u] ? s : kNegInf;
         s2[u][i] = s;
-        if (scores && part == 0) s_lds[i * kMaxChunk + it * kPerIter + u * TPW + tsub] = s;
-        raise = raise || (s > m2[i] + kLazy);
+        // every lane of the token holds s: all of them store it (same
+        // value, same address), which keeps the loop free of exec-mask
+        // branches around the store
+        s_lds[i * kMaxChunk + it * kPerIter + u * TPW + tsub] = s;
+        raise |= __ballot(s > m2[i] + kLazy);
       }
     }
-    if (__ballot(raise)) {
+    if (raise) {
 #pragma unroll
       for (int i = 0; i < G; ++i) {
         float mx = s2[0][i];
@@ -406,6 +425,9 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
         }
       }
     }
+  };
+  // Value sums of one iteration.
+  auto proc_v = [&](Rows<BITS, CPL>(&cur)[UNROLL]) {
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       uint32_t vx[NP];
@@ -428,10 +450,31 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
       }
     }
   };
+  auto proc = [&](Rows<BITS, CPL>(&cur)[UNROLL], int it) {
+    proc_k(cur, it);
+    proc_v(cur);
+  };
 
   // Software pipeline: the rows of the next PREFETCH iterations are loaded
-  // while the current one is computed.
-  if constexpr (PREFETCH == 0) {
+  // while the current one is computed.  PREFETCH < 0: half steps in the
+  // same registers -- the next iteration's keys are loaded as soon as the
+  // scores are done, its values as soon as the value sums are, so one half
+  // of the rows is always in flight without extra registers.
+  if constexpr (PREFETCH < 0) {
+    // (no branch around the loads, and scheduling barriers: a load issued
+    // early would need registers of its own)
+    for (int it = 0; it < n_iter; ++it) {
+      const bool live = it + 1 < n_iter;
+      proc_k(cur, it);
+      __builtin_amdgcn_sched_barrier(0);
+      load_part(std::integral_constant<int, 1>{}, cur, it + 1, live);
+      __builtin_amdgcn_sched_barrier(0);
+      proc_v(cur);
+      __builtin_amdgcn_sched_barrier(0);
+      load_part(std::integral_constant<int, 2>{}, cur, it + 1, live);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  } else if constexpr (PREFETCH == 0) {
     for (int it = 0; it < n_iter; ++it) {
       if (it > 0) load_it(cur, it);
       proc(cur, it);
@@ -742,7 +785,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
     const int t0 = start + it * kItTok;
     // --- scores of the four key tiles
     float s2[4][NSET];
-    bool raise = false;
+    uint64_t raise = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       uint32_t P[16];
@@ -774,11 +817,11 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         const float v2 = valid ? s * s2scale : kNegInf;
         s2[q][st] = v2;
         if (scores) s_lds[(qs + 4 * st) * kMaxChunk + (t0 - start) + 16 * q + n] = v2;  // replicas agree
-        raise = raise || (v2 > m_own[st] + kLazy);
+        raise |= __ballot(v2 > m_own[st] + kLazy);
       }
     }
     // --- lazy running max (per query; rare after the first tokens)
-    if (__ballot(raise)) {
+    if (raise) {
       float f[G];
 #pragma unroll
       for (int i = 0; i < G; ++i) f[i] = 1.0f;
@@ -910,19 +953,20 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   }
 }
 
-// Tuning: token tiles per lane per iteration and prefetch depth, for
-// low-bit (INT2/INT4) and high-bit (fp16/INT8) rows.
+// Tuning: token tiles per lane per iteration and prefetch depth (-1: the
+// half-step pipeline of attn_chunk), for low-bit (INT2/INT4) and high-bit
+// (fp16/INT8) rows.
 #ifndef MIKV_UNROLL_LOWBIT
 #define MIKV_UNROLL_LOWBIT 8
 #endif
 #ifndef MIKV_UNROLL_HIGHBIT
-#define MIKV_UNROLL_HIGHBIT 1
+#define MIKV_UNROLL_HIGHBIT 2
 #endif
 #ifndef MIKV_PREFETCH_LOWBIT
-#define MIKV_PREFETCH_LOWBIT 0
+#define MIKV_PREFETCH_LOWBIT -1
 #endif
 #ifndef MIKV_PREFETCH_HIGHBIT
-#define MIKV_PREFETCH_HIGHBIT 1
+#define MIKV_PREFETCH_HIGHBIT -1
 #endif
 template <int BITS>
 constexpr int unroll_for() { return BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL_HIGHBIT; }
@@ -966,7 +1010,21 @@ template <int HI, int LO, int G, bool SPLITQ>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
-  const int h = blockIdx.y, c = blockIdx.x;
+  // Block -> (head, chunk): first every head's importance-pool chunks and
+  // the retained-pool chunks that cannot be empty (nc_first per head), then
+  // the retained-pool chunks that may be (a wave that finds its chunk empty
+  // costs little at the end of the grid, but holds up the dispatch of the
+  // work behind it anywhere else).
+  const int n_first = gridDim.x / (A.nc_hi + A.nc_lo) * A.nc_first;  // blocks of the first part
+  int h, c;
+  if ((int)blockIdx.x < n_first) {
+    h = blockIdx.x / A.nc_first;
+    c = blockIdx.x % A.nc_first;
+  } else {
+    const int rest = A.nc_hi + A.nc_lo - A.nc_first, e = blockIdx.x - n_first;
+    h = e / rest;
+    c = A.nc_first + e % rest;
+  }
   __shared__ float s_lds[G * kMaxChunk];  // the chunk's scores, [G][kMaxChunk]
   if (c < A.nc_hi) {
     if (A.hi_pending) append_in_chunk<HI>(A, h, c);
@@ -1240,6 +1298,7 @@ __global__ __launch_bounds__(kBlock) void importance_kernel(float *acc, const fl
 // ---------------------------------------------------------------------------
 struct Plan {
   int chunk_hi, chunk_lo, nc_hi, nc_lo;
+  int nc_first;  // nc_hi + the retained-pool chunks that hold tokens whatever the split
 };
 
 int round_up(int64_t x, int m) { return (int)(((x + m - 1) / m) * m); }
@@ -1258,6 +1317,10 @@ Plan make_plan(const mikv_cache *c, int length) {
   p.chunk_lo = std::min(kMaxChunk, std::max(128, round_up(target / bl, 128)));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
   p.nc_lo = std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
+  // every token is in one of the pools, so at least length - cap_hi are in
+  // the retained one (only the dispatch order depends on this)
+  const int lo_min = std::max(0, std::min(span_lo, length - c->cap_hi));
+  p.nc_first = p.nc_hi + std::min(p.nc_lo, (lo_min + p.chunk_lo - 1) / p.chunk_lo);
   return p;
 }
 
@@ -1301,6 +1364,7 @@ AttnArgs make_args(const mikv_cache *c, const Plan &p, const uint16_t *q, const 
   A.chunk_lo = p.chunk_lo;
   A.nc_hi = p.nc_hi;
   A.nc_lo = p.nc_lo;
+  A.nc_first = p.nc_first;
   A.app = AppendArgs{};
   A.hi_pending = 0;
   return A;
@@ -1386,7 +1450,7 @@ int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, flags, ws);
   if (k_new) set_append(A, c, length, k_new, v_new, balance);
-  dim3 grid(p.nc_hi + p.nc_lo, n_heads_of(c));
+  dim3 grid((p.nc_hi + p.nc_lo) * n_heads_of(c));
   const int G = group_size_of(c);
   switch (c->hi_bits * 100 + c->lo_bits) {
     case 1602: launch_partial_g<16, 2>(A, G, grid, st); break;
