@@ -94,6 +94,10 @@ def cpu_baseline(wl, steps_inputs, budget_s: float):
             "s_per_step_per_head": round(el / max(done, 1) / len(heads), 4)}
 
 
+# The attention partial kernel's source files (its traffic record is keyed by them).
+KERNEL_SOURCES = ("attention.hip", "mikv_internal.h", "append_device.h", "select_device.h")
+
+
 def measured_traffic(workload: str):
     """HBM bytes per attention partial launch from the committed rocprofv3
     counter runs (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter
@@ -106,7 +110,7 @@ def measured_traffic(workload: str):
     with open(path) as f:
         rec = json.load(f)
     h = hashlib.sha256()
-    for name in ("attention.hip", "mikv_internal.h"):
+    for name in KERNEL_SOURCES:
         with open(os.path.join(ROOT, "paper_2402_18096_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     if rec.get("source_sha256") != h.hexdigest():
