@@ -584,7 +584,12 @@ __device__ inline float row_sum16(float v) {
   return v + dpp_mov<0x140>(v);
 }
 
-constexpr int kItTok = 64;                     // tokens per iteration: four key tiles, two value tiles
+#ifndef MIKV_INT2_KEY_TILES
+#define MIKV_INT2_KEY_TILES 4
+#endif
+constexpr int kKT = MIKV_INT2_KEY_TILES;  // 16-token key tiles per iteration (2 or 4)
+constexpr int kVT = kKT / 2;              // 32-token value tiles per iteration
+constexpr int kItTok = 16 * kKT;          // tokens per iteration
 // Operand element -> slot inside a lane group's 8 (and back): bits 0 and 1
 // swapped, the order the masked code pairs come out in.
 __host__ __device__ constexpr int tau8(int e) { return (e & 4) | ((e & 1) << 1) | ((e >> 1) & 1); }
@@ -624,47 +629,59 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   // One iteration's loads: key codes and parameter rows of the four key
   // tiles (the lane's value groups only), value codes of the two tiles.
   struct Ld {
-    uint32_t kc[4][2];
-    uint32_t kp[4][NG];
-    uint32_t vp[4][NGL];
-    uint32_t vc[2][8][2];
+    uint32_t kc[kKT][2];
+    uint32_t kp[kKT][NG];
+    uint32_t vp[kKT][NGL];
+    uint32_t vc[kVT][8][2];
   };
-  auto load = [&](Ld &d, int it) {
+  // KEYS: the key codes and parameters; VALS: the value codes and
+  // parameters.  With `live` false every load goes through an empty
+  // descriptor (zero, no memory access), so no branch is needed around it.
+  const rsrc_t r_none = make_rsrc(A.lo_k, 0u);
+  auto load = [&](Ld &d, int it, bool keys, bool vals, bool live) {
     const uint32_t t0 = (uint32_t)(start + it * kItTok);
+    const rsrc_t ak = live ? rk : r_none, av = live ? rv : r_none;
+    const rsrc_t akp = live ? rkp : r_none, avp = live ? rvp : r_none;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < kKT; ++q) {
       const uint32_t slot = t0 + 16 * q + n;
-      auto kc = __builtin_amdgcn_raw_buffer_load_b64(rk, slot * 32u + 8u * a, 0, 0);
-      d.kc[q][0] = kc[0];
-      d.kc[q][1] = kc[1];
-      if constexpr (NG == 4) {
-        auto kp = __builtin_amdgcn_raw_buffer_load_b128(rkp, slot * 16u, 0, 0);
+      if (keys) {
+        auto kc = __builtin_amdgcn_raw_buffer_load_b64(ak, slot * 32u + 8u * a, 0, 0);
+        d.kc[q][0] = kc[0];
+        d.kc[q][1] = kc[1];
+        if constexpr (NG == 4) {
+          auto kp = __builtin_amdgcn_raw_buffer_load_b128(akp, slot * 16u, 0, 0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) d.kp[q][j] = kp[j];
-      } else if constexpr (NG == 2) {
-        auto kp = __builtin_amdgcn_raw_buffer_load_b64(rkp, slot * 8u, 0, 0);
-        d.kp[q][0] = kp[0];
-        d.kp[q][1] = kp[1];
-      } else {
-        d.kp[q][0] = __builtin_amdgcn_raw_buffer_load_b32(rkp, slot * 4u, 0, 0);
+          for (int j = 0; j < 4; ++j) d.kp[q][j] = kp[j];
+        } else if constexpr (NG == 2) {
+          auto kp = __builtin_amdgcn_raw_buffer_load_b64(akp, slot * 8u, 0, 0);
+          d.kp[q][0] = kp[0];
+          d.kp[q][1] = kp[1];
+        } else {
+          d.kp[q][0] = __builtin_amdgcn_raw_buffer_load_b32(akp, slot * 4u, 0, 0);
+        }
       }
+      if (vals) {
 #pragma unroll
-      for (int j = 0; j < NGL; ++j)
-        d.vp[q][j] = __builtin_amdgcn_raw_buffer_load_b32(rvp, (slot * NG + (uint32_t)((rho + R * j) % NG)) * 4u, 0, 0);
+        for (int j = 0; j < NGL; ++j)
+          d.vp[q][j] = __builtin_amdgcn_raw_buffer_load_b32(avp, (slot * NG + (uint32_t)((rho + R * j) % NG)) * 4u, 0, 0);
+      }
     }
+    if (vals) {
 #pragma unroll
-    for (int vt = 0; vt < 2; ++vt) {
-      const uint32_t tile = (t0 >> 5) + vt;
+      for (int vt = 0; vt < kVT; ++vt) {
+        const uint32_t tile = (t0 >> 5) + vt;
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) {
-        auto vc = __builtin_amdgcn_raw_buffer_load_b64(rv, tile * 1024u + (uint32_t)(4 * nb + n / 4) * 32u + 8u * a, 0, 0);
-        d.vc[vt][nb][0] = vc[0];
-        d.vc[vt][nb][1] = vc[1];
+        for (int nb = 0; nb < 8; ++nb) {
+          auto vc = __builtin_amdgcn_raw_buffer_load_b64(av, tile * 1024u + (uint32_t)(4 * nb + n / 4) * 32u + 8u * a, 0, 0);
+          d.vc[vt][nb][0] = vc[0];
+          d.vc[vt][nb][1] = vc[1];
+        }
       }
     }
   };
   Ld cur;
-  if (n_iter > 0) load(cur, 0);
+  if (n_iter > 0) load(cur, 0, true, true, true);
 
   // zero the weight rows (rows past 2G are never written)
   {
@@ -780,14 +797,16 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   for (int nb = 0; nb < 8; ++nb) CV[nb] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
   const uint32_t mk = 0x00030003u << (2 * (n & 3));  // value field of this lane's column
 
+  // Half-step pipeline (as in attn_chunk): the next iteration's keys are
+  // loaded once the scores are done, its values once the value MFMAs are.
   for (int it = 0; it < n_iter; ++it) {
-    if (it > 0) load(cur, it);
+    const bool live = it + 1 < n_iter;
     const int t0 = start + it * kItTok;
     // --- scores of the four key tiles
-    float s2[4][NSET];
+    float s2[kKT][NSET];
     uint64_t raise = 0;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < kKT; ++q) {
       uint32_t P[16];
 #pragma unroll
       for (int w = 0; w < 2; ++w) {
@@ -827,7 +846,9 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       for (int i = 0; i < G; ++i) f[i] = 1.0f;
 #pragma unroll
       for (int st = 0; st < NSET; ++st) {
-        float mx = fmaxf(fmaxf(s2[0][st], s2[1][st]), fmaxf(s2[2][st], s2[3][st]));
+        float mx = s2[0][st];
+#pragma unroll
+        for (int q = 1; q < kKT; ++q) mx = fmaxf(mx, s2[q][st]);
         mx = row_max16(mx);
         float ra[4];
 #pragma unroll
@@ -868,9 +889,12 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         for (int nb = 0; nb < 8; ++nb) CV[nb][r] *= fr;
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
+    load(cur, it + 1, true, false, live);
+    __builtin_amdgcn_sched_barrier(0);
     // --- weights e * alpha into LDS (the A layout of the value MFMAs)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < kKT; ++q) {
       const int p = 16 * q + n, vt = p >> 5, u = p & 31;
       const int gv = u >> 3, ei = tau8(u & 7);
 #pragma unroll
@@ -895,7 +919,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     // --- value MFMAs
 #pragma unroll
-    for (int vt = 0; vt < 2; ++vt) {
+    for (int vt = 0; vt < kVT; ++vt) {
       h8_t AV[NG];
 #pragma unroll
       for (int gm = 0; gm < NG; ++gm) AV[gm] = *reinterpret_cast<const h8_t *>(w_lds + w_index(gm, vt, n, a, 0));
@@ -905,6 +929,9 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         CV[nb] = mfma32(AV[(16 * nb) / GROUP], pack_h8(d0 & mk, (d0 >> 8) & mk, d1 & mk, (d1 >> 8) & mk), CV[nb]);
       }
     }
+    __builtin_amdgcn_sched_barrier(0);
+    load(cur, it + 1, false, true, live);
+    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -976,7 +1003,7 @@ constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PR
 // Query heads per KV head from which a lane holds 16 channels instead of 32
 // (fewer accumulators per lane at larger GQA groups).
 #ifndef MIKV_NARROW_FROM_G
-#define MIKV_NARROW_FROM_G 8
+#define MIKV_NARROW_FROM_G 4
 #endif
 #ifndef MIKV_WAVES_PER_EU
 #define MIKV_WAVES_PER_EU 1
