@@ -53,6 +53,10 @@ constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLazy = 8.0f;       // raise the running max only past this (log2 units)
 constexpr int kMaxChunk = 1024;     // tokens per chunk at most (the chunk's scores are held in LDS)
+// Tokens per chunk at most for G query heads per KV head: the chunk's
+// scores (G x chunk fp32) stay within 8 KiB of LDS, so LDS does not bound
+// the waves per CU below what the registers allow.
+__host__ __device__ constexpr int max_chunk(int G) { return G <= 2 ? kMaxChunk : 2048 / G; }
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
@@ -268,9 +272,9 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   }
 
   constexpr int kPerIter = kWaves * TPW * UNROLL;
-  // chunks are whole multiples of 128 tokens, at most kMaxChunk: an
+  // chunks are whole multiples of 128 tokens, at most max_chunk(G): an
   // iteration never runs past the LDS score buffer
-  static_assert(128 % kPerIter == 0 && kMaxChunk % 128 == 0, "iteration must divide 128 tokens");
+  static_assert(128 % kPerIter == 0 && max_chunk(G) % 128 == 0, "iteration must divide 128 tokens");
   constexpr int kSeg = Rows<BITS, CPL>::KW * 4;  // bytes of one lane's row segment
   const int n_iter = end > start ? (end - start + kPerIter - 1) / kPerIter : 0;
   const int first = start + wave * TPW * UNROLL + tsub;  // this lane's token in iteration 0, u = 0
@@ -404,7 +408,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
         // every lane of the token holds s: all of them store it (same
         // value, same address), which keeps the loop free of exec-mask
         // branches around the store
-        s_lds[i * kMaxChunk + it * kPerIter + u * TPW + tsub] = s;
+        s_lds[i * max_chunk(G) + it * kPerIter + u * TPW + tsub] = s;
         raise |= __ballot(s > m2[i] + kLazy);
       }
     }
@@ -503,7 +507,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int i = 0; i < G; ++i)
-      for (int j = lane; j < end - start; j += 64) score_row[i][start + j] = s_lds[i * kMaxChunk + j];
+      for (int j = lane; j < end - start; j += 64) score_row[i][start + j] = s_lds[i * max_chunk(G) + j];
   }
 
   // Undo the code scaling, add the beta part, merge the lanes of equal
@@ -585,7 +589,7 @@ __device__ inline float row_sum16(float v) {
 }
 
 #ifndef MIKV_INT2_KEY_TILES
-#define MIKV_INT2_KEY_TILES 4
+#define MIKV_INT2_KEY_TILES 2
 #endif
 constexpr int kKT = MIKV_INT2_KEY_TILES;  // 16-token key tiles per iteration (2 or 4)
 constexpr int kVT = kKT / 2;              // 32-token value tiles per iteration
@@ -619,7 +623,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   const int end = min(start + A.chunk_lo, n_pool);
   const int n_iter = end > start ? (end - start + kItTok - 1) / kItTok : 0;
   float *scores = A.scores_lo;
-  const float s2scale = A.scale * kLog2e;
+  const float s2scale_q = __builtin_ldexpf(A.scale * kLog2e, 24);
 
   const rsrc_t rk = make_rsrc(A.lo_k + (int64_t)h * cap * 32, (uint32_t)n_pool * 32u);
   const rsrc_t rv = make_rsrc(A.lo_v + (int64_t)h * cap * 32, (uint32_t)((n_pool + 31) / 32) * 1024u);
@@ -771,7 +775,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       float v = all[0][gm];
 #pragma unroll
       for (int s3 = 1; s3 < QS; ++s3) v = qs == s3 ? all[s3][gm] : v;
-      qsl[st][gm] = v;
+      qsl[st][gm] = __builtin_ldexpf(v, -24);  // 2^-24: the scale of the scores below
     }
   }
 
@@ -826,16 +830,17 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             C = mfma32(AK[st][pt][i], pack_h8(P[4 * i], P[4 * i + 1], P[4 * i + 2], P[4 * i + 3]), C);
+        // 2^-24 times the folded score (the fp16 scale and zero enter
+        // mixed-precision FMAs as stored; the power of two is in the scale)
         float s = 0.0f;
 #pragma unroll
         for (int gm = 0; gm < NG; ++gm) {
-          const uint32_t kw = cur.kp[q][gm];
-          const float ka = __builtin_ldexpf(f16_to_f32((uint16_t)(kw & 0xffffu)), 24);
-          s = fmaf(ka, C[gm], fmaf(f16_to_f32((uint16_t)(kw >> 16)), qsl[st][gm], s));
+          const half2_t kab = as_h2(cur.kp[q][gm]);
+          s = fmaf((float)kab.x, C[gm], fmaf((float)kab.y, qsl[st][gm], s));
         }
-        const float v2 = valid ? s * s2scale : kNegInf;
+        const float v2 = valid ? s * s2scale_q : kNegInf;
         s2[q][st] = v2;
-        if (scores) s_lds[(qs + 4 * st) * kMaxChunk + (t0 - start) + 16 * q + n] = v2;  // replicas agree
+        if (scores) s_lds[(qs + 4 * st) * max_chunk(G) + (t0 - start) + 16 * q + n] = v2;  // replicas agree
         raise |= __ballot(v2 > m_own[st] + kLazy);
       }
     }
@@ -905,9 +910,9 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #pragma unroll
         for (int j = 0; j < NGL; ++j) {
           const int gm = (rho + R * j) % NG;
-          const uint32_t vpw = cur.vp[q][j];
-          const float w = e * f16_to_f32((uint16_t)(vpw & 0xffffu));
-          bs_l[st][j] = fmaf(e * dup[j], f16_to_f32((uint16_t)(vpw >> 16)), bs_l[st][j]);
+          const half2_t vab = as_h2(cur.vp[q][j]);  // (alpha, beta) of the value group
+          const float w = fmaf(e, (float)vab.x, 0.0f);
+          bs_l[st][j] = fmaf(e * dup[j], (float)vab.y, bs_l[st][j]);
           const _Float16 wh = (_Float16)w, wl = (_Float16)(w - (float)wh);
           w_lds[w_index(gm, vt, 2 * iq, gv, ei)] = wh;
           w_lds[w_index(gm, vt, 2 * iq + 1, gv, ei)] = wl;
@@ -943,7 +948,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #pragma unroll
     for (int i = 0; i < G; ++i) {
       float *row = scores + (int64_t)(qh0 + i) * cap;
-      for (int j = lane; j < end - start; j += 64) row[start + j] = s_lds[i * kMaxChunk + j];
+      for (int j = lane; j < end - start; j += 64) row[start + j] = s_lds[i * max_chunk(G) + j];
     }
   }
   // Normalisers and zero terms per (query, group), wave-uniform.
@@ -1052,7 +1057,7 @@ void attn_partial_kernel(AttnArgs A) {
     h = e / rest;
     c = A.nc_first + e % rest;
   }
-  __shared__ float s_lds[G * kMaxChunk];  // the chunk's scores, [G][kMaxChunk]
+  __shared__ float s_lds[G * max_chunk(G)];  // the chunk's scores, [G][max_chunk(G)]
   if (c < A.nc_hi) {
     if (A.hi_pending) append_in_chunk<HI>(A, h, c);
     attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
@@ -1340,8 +1345,9 @@ Plan make_plan(const mikv_cache *c, int length) {
   // units balance the CUs best), at least 16 KiB so the per-chunk merge
   // stays cheap.  Chunks are whole wave iterations (128 tokens).
   int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, MIKV_CHUNK_KB << 10), 16 << 10);
-  p.chunk_hi = std::min(kMaxChunk, std::max(128, round_up(target / bh, 128)));
-  p.chunk_lo = std::min(kMaxChunk, std::max(128, round_up(target / bl, 128)));
+  const int cmax = max_chunk(group_size_of(c));
+  p.chunk_hi = std::min(cmax, std::max(128, round_up(target / bh, 128)));
+  p.chunk_lo = std::min(cmax, std::max(128, round_up(target / bl, 128)));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
   p.nc_lo = std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
   // every token is in one of the pools, so at least length - cap_hi are in
