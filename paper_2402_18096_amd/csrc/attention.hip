@@ -1000,8 +1000,13 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #ifndef MIKV_PREFETCH_HIGHBIT
 #define MIKV_PREFETCH_HIGHBIT -1
 #endif
+// INT4 rows are twice the INT2 ones: half the tiles per iteration keep the
+// same bytes in flight and the registers of one more wave per SIMD.
+#ifndef MIKV_UNROLL_INT4
+#define MIKV_UNROLL_INT4 4
+#endif
 template <int BITS>
-constexpr int unroll_for() { return BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL_HIGHBIT; }
+constexpr int unroll_for() { return BITS == 4 ? MIKV_UNROLL_INT4 : BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL_HIGHBIT; }
 template <int BITS>
 constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PREFETCH_HIGHBIT; }
 
