@@ -119,11 +119,12 @@ const char *mikv_last_error(void);
  *   balance[b, h, c] = sqrt( max_{t, i in group(h)} |q[b, i, t, c]| / max_t |k[b, h, t, c]| )
  * over the prefill prompt, in fp32 (correctly rounded divide and square
  * root); 1 where either maximum is 0.
- *   q_prefill fp16 [B, Hq, T, 128]; k_prefill fp16 [B, Hkv, T, 128];
+ *   q_prefill fp16 [B, Hq, T, 128]; k_prefill fp16 [B, Hkv, T, 128], both
+ *             16-byte aligned;
  *   balance   fp32 [B, Hkv, 128] (output);
  *   workspace device bytes, at least mikv_balance_workspace_size(B, Hkv, T).
- * Errors: INVALID_ARG for null pointers, T < 1, Hq % Hkv != 0; UNSUPPORTED
- * for head_dim != 128; CAPACITY for a too-small workspace.
+ * Errors: INVALID_ARG for null or misaligned pointers, T < 1, Hq % Hkv != 0;
+ * UNSUPPORTED for head_dim != 128; CAPACITY for a too-small workspace.
  */
 size_t mikv_balance_workspace_size(int32_t batch, int32_t kv_heads, int32_t tokens);
 int mikv_balance_channels(const uint16_t *q_prefill, const uint16_t *k_prefill, int32_t batch,

@@ -88,6 +88,9 @@ def test_null_pointers_and_capacity():
     assert L.mikv_select_prefill(None, 1, 4, 1, 1, None, None) == 1
     assert L.mikv_balance_channels(ctypes.c_void_p(1), ctypes.c_void_p(1), 1, 4, 4, 8, 64, ctypes.c_void_p(1),
                                    ctypes.c_void_p(1), 1 << 20, None) == 2
+    # 16-byte alignment of the prefill rows (checked on the host, nothing launched)
+    assert L.mikv_balance_channels(ctypes.c_void_p(0x1002), ctypes.c_void_p(0x1000), 1, 4, 4, 8, 128,
+                                   ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), 1 << 20, None) == 1
     assert L.mikv_importance_update(ctypes.byref(_desc()), 4, None, None) == 1
     qk = ctypes.c_void_p(0x1000)
     assert L.mikv_quantize_kv(ctypes.byref(_desc()), qk, qk, None, 10, 8, None, None, None, 0, None) == 3
