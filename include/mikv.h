@@ -257,21 +257,22 @@ int mikv_select_prefill(const float *scores, int32_t n_heads, int32_t length, in
  *   4. mikv_select_topk(k_heavy, window).
  *   q fp16 [B, Hq, 128]; k_new, v_new fp16 [B, Hkv, 128]; other arguments as
  *   in the calls above (probs_hi is required unless MIKV_ATTN_ACCUMULATE).
- * With MIKV_ATTN_ACCUMULATE and at most 512 (sequence, KV head) pairs the
- * step is two launches: step 1 runs inside the partial phase of step 2 (the
- * wave that attends over the new token's slot writes it first), and steps
- * 2 (finalize phase), 3 and 4 run as one launch, whose block that updates a
- * head's importance scores then runs that head's re-rank.  n_hi counts the
- * new token from the end of the step on; results are those of the four
- * calls.
+ * With MIKV_ATTN_ACCUMULATE, step 1 runs inside the partial phase of step 2
+ * (the wave that attends over the new token's slot writes it first), and
+ * with at most 512 (sequence, KV head) pairs steps 2 (finalize phase), 3
+ * and 4 run as one launch, whose block that updates a head's importance
+ * scores then runs that head's re-rank (two launches in all; three above
+ * 512 pairs).  n_hi counts the new token from the end of the step on;
+ * results are those of the four calls.
  *   workspace    at least mikv_decode_step_workspace_size(c, length) bytes
  *                (the attention's and the select's workspaces); its
  *                contents need not be initialised;
  *   phase_events NULL, or 6 hipEvent_t (entries may be NULL) recorded on
  *                `stream` before step 1 and after steps 1, 2 (partial
  *                phase), 2 (finalize phase), 3 and 4, for profiling (with
- *                two launches the first two events both mark the start of
- *                the first launch and the last three the end of the second).
+ *                the append folded the first two events both mark the start
+ *                of the partial phase; with the fused launch the last three
+ *                mark its end).
  * Errors: those of the four calls, checked before the first launch where the
  * host can check them.
  */

@@ -1547,15 +1547,16 @@ extern "C" int mikv_decode_attention_partial(const mikv_cache *c, int32_t length
                         (hipStream_t)stream);
 }
 
-extern "C" int mikv_decode_attention_finalize(const mikv_cache *c, int32_t length, const uint16_t *q,
-                                              const float *balance, float scale, float *out, float *probs_hi,
-                                              float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
-                                              void *stream) {
+namespace mikv {
+
+int decode_finalize(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
+                    float *out, float *probs_hi, float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
+                    bool appended, hipStream_t st) {
   int rc = check_attention_args(c, length, q, balance, out, ws, ws_bytes, "mikv_decode_attention_finalize");
   if (rc) return rc;
   Plan p = make_plan(c, length);
   AttnArgs A = make_args(c, p, q, balance, scale, out, probs_hi, probs_lo, flags, ws);
-  hipStream_t st = (hipStream_t)stream;
+  A.hi_pending = appended ? 1 : 0;
   const int acc = (flags & MIKV_ATTN_ACCUMULATE) ? 1 : 0;
   // probability tiles: importance pool when its probabilities are emitted or
   // accumulated, retained pool when its probabilities are emitted
@@ -1570,6 +1571,16 @@ extern "C" int mikv_decode_attention_finalize(const mikv_cache *c, int32_t lengt
     default: hipLaunchKernelGGL(attn_finalize_kernel<8>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;
   }
   return check_launch("mikv_decode_attention_finalize");
+}
+
+}  // namespace mikv
+
+extern "C" int mikv_decode_attention_finalize(const mikv_cache *c, int32_t length, const uint16_t *q,
+                                              const float *balance, float scale, float *out, float *probs_hi,
+                                              float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
+                                              void *stream) {
+  return decode_finalize(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, ws_bytes, false,
+                         (hipStream_t)stream);
 }
 
 extern "C" int mikv_decode_attention(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance,

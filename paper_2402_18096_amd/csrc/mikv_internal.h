@@ -35,6 +35,14 @@ int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const
 int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
                            float *out, float *probs_hi, float *probs_lo, void *ws, size_t ws_bytes, int32_t k_heavy,
                            int32_t window, void *sel_ws, bool appended, hipStream_t st);
+// The separate finalize and re-rank launches of the decode step (caches with
+// many heads), with the same meaning of `appended` (attention.hip,
+// select.hip).
+int decode_finalize(const mikv_cache *c, int32_t length, const uint16_t *q, const float *balance, float scale,
+                    float *out, float *probs_hi, float *probs_lo, int32_t flags, void *ws, size_t ws_bytes,
+                    bool appended, hipStream_t st);
+int select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window, void *ws, size_t ws_bytes,
+                bool appended, hipStream_t st);
 
 inline int group_size_of(const mikv_cache *c) { return c->q_heads / c->kv_heads; }
 inline int n_heads_of(const mikv_cache *c) { return c->batch * c->kv_heads; }

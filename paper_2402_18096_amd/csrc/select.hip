@@ -52,8 +52,10 @@ extern "C" size_t mikv_select_workspace_size(const mikv_cache *c) {
   return (size_t)2 * 4 * (size_t)c->batch * c->kv_heads * (size_t)std::max(c->cap_hi, 1);
 }
 
-extern "C" int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window, void *ws,
-                                size_t ws_bytes, void *stream) {
+namespace mikv {
+
+int select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window, void *ws, size_t ws_bytes,
+                bool appended, hipStream_t st) {
   int rc = validate_cache(c);
   if (rc) return rc;
   if (k_heavy < 0 || window < 0) return set_error(MIKV_ERR_INVALID_ARG, "mikv_select_topk: negative k_heavy/window");
@@ -63,8 +65,8 @@ extern "C" int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_h
   if (!ws || ws_bytes < mikv_select_workspace_size(c))
     return set_error(MIKV_ERR_CAPACITY, "mikv_select_topk: workspace too small");
   SelArgs A = make_sel_args(c, length, k_heavy, window, ws);
+  A.pending = appended ? 1 : 0;
   const int NH = n_heads_of(c);
-  hipStream_t st = (hipStream_t)stream;
   switch (c->hi_bits * 100 + c->lo_bits) {
     case 1602: launch_select<16, 2>(A, NH, st); break;
     case 1604: launch_select<16, 4>(A, NH, st); break;
@@ -74,6 +76,13 @@ extern "C" int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_h
     default: launch_select<8, 8>(A, NH, st); break;
   }
   return check_launch("mikv_select_topk");
+}
+
+}  // namespace mikv
+
+extern "C" int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window, void *ws,
+                                size_t ws_bytes, void *stream) {
+  return select_topk(c, length, k_heavy, window, ws, ws_bytes, false, (hipStream_t)stream);
 }
 
 extern "C" int mikv_select_prefill(const float *scores, int32_t n_heads, int32_t length, int32_t k_heavy,

@@ -135,6 +135,7 @@ struct SelArgs {
   int cap_hi, cap_lo, max_len, group;
   int length, k_heavy, window;
   int v_tiled;  // 2-bit values in the tiled layout (int2_values_tiled)
+  int pending;  // n_hi does not yet count the step's appended token (slot n_hi holds it)
 };
 
 // Decode the 32 channels [part*32, part*32+32) of an importance-pool row.
@@ -427,14 +428,15 @@ __device__ void select_finish(const SelArgs &A, int h, int n, int n_lo0, const S
 // Re-rank and demote for head h; the whole block (kSel threads) takes part.
 template <int HI_BITS, int LO_BITS>
 __device__ void select_head(const SelArgs &A, int h) {
-  const int n = __builtin_amdgcn_readfirstlane(A.n_hi[h]);
+  const int n_mem = __builtin_amdgcn_readfirstlane(A.n_hi[h]);
+  const int n = n_mem + (A.pending && n_mem < A.cap_hi ? 1 : 0);
   const int n_lo0 = __builtin_amdgcn_readfirstlane(A.n_lo[h]);
   SelScan sc;
   select_scan(A, h, 0, n, A.length - A.window, sc);
   // The last slot fills the hole of a demoted token: fetch it now, its
   // latency then hides behind the reductions.
   const SlotData<HI_BITS> last = n > 0 ? load_slot<HI_BITS>(A, h, n - 1) : SlotData<HI_BITS>{};
-  select_finish<HI_BITS, LO_BITS>(A, h, n, n_lo0, sc, last);
+  select_finish<HI_BITS, LO_BITS>(A, h, n, n_lo0, sc, last, A.pending != 0);
 }
 
 // Arguments of a select for the cache `c` (host side).
@@ -464,6 +466,7 @@ inline SelArgs make_sel_args(const mikv_cache *c, int length, int k_heavy, int w
   A.k_heavy = k_heavy;
   A.window = window;
   A.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
+  A.pending = 0;
   return A;
 }
 

@@ -65,6 +65,22 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
     mark(5);
     return MIKV_OK;
   }
+  if (fused) {
+    // Three launches: partial phase with the append, finalize with the
+    // importance update, re-rank (which counts the new token into n_hi).
+    mark(1);
+    rc = decode_partial(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws, k_new, v_new, st);
+    if (rc) return rc;
+    mark(2);
+    rc = decode_finalize(c, length, q, balance, scale, out, probs_hi, probs_lo, flags, ws, attn_ws, true, st);
+    if (rc) return rc;
+    mark(3);
+    mark(4);
+    rc = select_topk(c, length, k_heavy, window, ws + attn_ws, workspace_bytes - attn_ws, true, st);
+    if (rc) return rc;
+    mark(5);
+    return MIKV_OK;
+  }
   rc = mikv_quantize_kv(c, k_new, v_new, balance, length - 1, 1, nullptr, nullptr, nullptr, 0, stream);
   if (rc) return rc;
   mark(1);
@@ -76,10 +92,8 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
                                       stream);
   if (rc) return rc;
   mark(3);
-  if (!fused) {
-    rc = mikv_importance_update(c, length, probs_hi, stream);
-    if (rc) return rc;
-  }
+  rc = mikv_importance_update(c, length, probs_hi, stream);
+  if (rc) return rc;
   mark(4);
   rc = mikv_select_topk(c, length, k_heavy, window, ws + attn_ws, workspace_bytes - attn_ws, stream);
   if (rc) return rc;
