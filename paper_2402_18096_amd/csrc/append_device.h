@@ -95,19 +95,19 @@ __device__ inline void append_row(const AppendArgs &P, int h, int slot, int lane
   const int is_v = lane8 >> 2, lane4 = lane8 & 3;
   const float *bal = (!is_v && P.balance) ? P.balance + (int64_t)h * kHeadDim + lane4 * 32 : nullptr;
   float x[32];
-  load_row_segment((is_v ? P.v : P.k) + (int64_t)h * kHeadDim + lane4 * 32, bal, x);
+  load_row_segment(lane_pick(is_v, P.v, P.k) + (int64_t)h * kHeadDim + lane4 * 32, bal, x);
   const int64_t row = (int64_t)h * P.cap_hi + slot;
   if constexpr (HI_BITS == 16) {
     uint32_t w[16];
 #pragma unroll
     for (int c = 0; c < 16; ++c) w[c] = pack_f16x2(x[2 * c], x[2 * c + 1]);
-    uint4 *d4 = reinterpret_cast<uint4 *>((is_v ? P.hi_v : P.hi_k) + (row * kHeadDim + lane4 * 32) * 2);
+    uint4 *d4 = reinterpret_cast<uint4 *>(lane_pick(is_v, P.hi_v, P.hi_k) + (row * kHeadDim + lane4 * 32) * 2);
 #pragma unroll
     for (int i = 0; i < 4; ++i) d4[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
   } else {
     const int ng = kHeadDim / P.group;
-    uint8_t *dst = (is_v ? P.hi_v : P.hi_k) + row * kHeadDim + lane4 * 32;
-    uint32_t *par = (is_v ? P.hi_vp : P.hi_kp) + row * ng + (lane4 * 32) / P.group;
+    uint8_t *dst = lane_pick(is_v, P.hi_v, P.hi_k) + row * kHeadDim + lane4 * 32;
+    uint32_t *par = lane_pick(is_v, P.hi_vp, P.hi_kp) + row * ng + (lane4 * 32) / P.group;
     quantize_segment<8>(x, P.group, lane4, dst, par, true);
   }
   if (lane8 == 0) {

@@ -1183,7 +1183,13 @@ __device__ inline void prob_tile_store(const AttnArgs &A, int h, int qh0, bool i
 template <int G>
 __device__ inline void merge_output(const AttnArgs &A, int qh0, int nc, const float M[G], const float inv[G]) {
   constexpr int S = 8 / G;
-  const int q4 = threadIdx.x % 32, i = (threadIdx.x / 32) % G, s = threadIdx.x / (32 * G);
+  // Up to four query heads, a wave works on one head (i wave-uniform, so
+  // picking its statistics is a scalar select, not a per-lane indexed array);
+  // eight heads take two per wave.
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int q4 = lane & 31;
+  const int i = G <= 4 ? __builtin_amdgcn_readfirstlane(wave % G) : (threadIdx.x / 32) % G;
+  const int s = G <= 4 ? (wave / G) * 2 + (lane >> 5) : threadIdx.x / (32 * G);
   const float *rec = A.partials + (int64_t)(qh0 + i) * nc * kRec;
   float Mi = M[0], invi = inv[0];
 #pragma unroll
@@ -1193,23 +1199,36 @@ __device__ inline void merge_output(const AttnArgs &A, int qh0, int nc, const fl
       invi = inv[j];
     }
   float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-#pragma unroll 8
-  for (int r = s; r < nc; r += S) {
-    const float *rr = rec + (int64_t)r * kRec;
-    const float mr = rr[0];
-    const float4 o = reinterpret_cast<const float4 *>(rr + kRecO)[q4];
-    const float w = mr == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(mr - Mi);
-    v.x = fmaf(o.x, w, v.x);
-    v.y = fmaf(o.y, w, v.y);
-    v.z = fmaf(o.z, w, v.z);
-    v.w = fmaf(o.w, w, v.w);
+  // RB records per thread and batch, all loaded before any is used (a
+  // missing record reads record 0 and gets weight 0): one memory round trip
+  // per batch (a plain loop waits for every record in turn)
+  constexpr int RB = 8;
+  for (int r0 = s; r0 < nc; r0 += RB * S) {
+    float mr[RB];
+    float4 o[RB];
+#pragma unroll
+    for (int k = 0; k < RB; ++k) {
+      const int r = r0 + k * S;
+      const float *rr = rec + (int64_t)(r < nc ? r : 0) * kRec;
+      mr[k] = r < nc ? rr[0] : kNegInf;
+      o[k] = reinterpret_cast<const float4 *>(rr + kRecO)[q4];
+    }
+#pragma unroll
+    for (int k = 0; k < RB; ++k) {
+      const float w = mr[k] == kNegInf ? 0.0f : __builtin_amdgcn_exp2f(mr[k] - Mi);
+      v.x = fmaf(o[k].x, w, v.x);
+      v.y = fmaf(o[k].y, w, v.y);
+      v.z = fmaf(o[k].z, w, v.z);
+      v.w = fmaf(o[k].w, w, v.w);
+    }
   }
   __shared__ float4 s_o[kBlock];
-  s_o[threadIdx.x] = v;
+  const int slot = (s * G + i) * 32 + q4;  // LDS by (split, head, channels)
+  s_o[slot] = v;
   __syncthreads();
   if (s == 0) {
     for (int s2 = 1; s2 < S; ++s2) {
-      const float4 u = s_o[threadIdx.x + s2 * 32 * G];
+      const float4 u = s_o[slot + s2 * 32 * G];
       v.x += u.x;
       v.y += u.y;
       v.z += u.z;
@@ -1232,13 +1251,17 @@ void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi, int tiles_lo
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
+  float M[G], inv[G];
+  if (c == 0) {  // the merge holds no tile
+    head_stats<G>(A, qh0, nc, M, inv);
+    merge_output<G>(A, qh0, nc, M, inv);
+    return;
+  }
   const int tile = c - 1;
   const bool is_hi = tile < tiles_hi;
-  const bool has_tile = c > 0 && (is_hi || tile - tiles_hi < tiles_lo);
+  const bool has_tile = is_hi || tile - tiles_hi < tiles_lo;
   const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, is_hi, is_hi ? tile : tile - tiles_hi, has_tile, accumulate);
-  float M[G], inv[G];
   head_stats<G>(A, qh0, nc, M, inv);
-  if (c == 0) merge_output<G>(A, qh0, nc, M, inv);
   if (has_tile) prob_tile_store<G>(A, h, qh0, is_hi, accumulate, T, M, inv);
 }
 
@@ -1258,15 +1281,18 @@ __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
   const int qh0 = b * A.q_heads + kvh * G;
   const int nc = A.nc_hi + A.nc_lo;
-  if (c > 0) {
-    const bool has_tile = c >= 2 && c - 2 < tiles_lo;
+  if (c == 1) {  // the merge holds no tile
+    float M[G], inv[G];
+    head_stats<G>(A, qh0, nc, M, inv);
+    merge_output<G>(A, qh0, nc, M, inv);
+    return;
+  }
+  if (c > 1) {
+    const bool has_tile = c - 2 < tiles_lo;
     const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, false, c - 2, has_tile, false);
     float M[G], inv[G];
     head_stats<G>(A, qh0, nc, M, inv);
-    if (c == 1)
-      merge_output<G>(A, qh0, nc, M, inv);
-    else if (has_tile)
-      prob_tile_store<G>(A, h, qh0, false, false, T, M, inv);
+    if (has_tile) prob_tile_store<G>(A, h, qh0, false, false, T, M, inv);
     return;
   }
   // Everything the re-rank reads besides the new scores is loaded together

@@ -145,6 +145,20 @@ __device__ inline uint32_t encode(float x, const GroupParams &p, int bits) {
 // retained pools shared by two or more query heads (GQA).  With one query
 // head per KV head the values stay token-major (the vector path reads a
 // token's row per lane).
+// c ? a : b for wave-uniform pointers (argument fields) and a per-lane
+// condition, selected as values: a select between two fields of an argument
+// struct can otherwise become a per-lane indexed load from the struct, which
+// the compiler serves by copying the whole struct to scratch memory.
+template <class T>
+__device__ inline T *lane_pick(bool c, T *a, T *b) {
+  const uint64_t ua = (uint64_t)a, ub = (uint64_t)b;
+  const uint64_t fa = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(ua >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ua);
+  const uint64_t fb = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(ub >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)ub);
+  return reinterpret_cast<T *>(c ? fa : fb);
+}
+
 __host__ __device__ inline bool int2_values_tiled(int lo_bits, int q_heads, int kv_heads) {
   return lo_bits == 2 && q_heads >= 2 * kv_heads;
 }

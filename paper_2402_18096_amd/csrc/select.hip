@@ -10,8 +10,9 @@ namespace mikv {
 
 namespace {
 
+// (Register budget: five blocks per CU, so 1280 heads take one round.)
 template <int HI_BITS, int LO_BITS>
-__global__ __launch_bounds__(kSel) void select_kernel(SelArgs A) {
+__global__ __launch_bounds__(kSel) __attribute__((amdgpu_waves_per_eu(5))) void select_kernel(SelArgs A) {
   select_head<HI_BITS, LO_BITS>(A, blockIdx.x);
 }
 

@@ -201,13 +201,13 @@ __device__ inline void store_lo_segment(const SelArgs &A, int h, int64_t lslot, 
   if (LO_BITS == 2 && is_v && A.v_tiled) {
     store_int2_v(A.lo_v + (int64_t)h * A.cap_lo * (kHeadDim / 4), lslot - (int64_t)h * A.cap_lo, part, w);
   } else {
-    uint32_t *codes = reinterpret_cast<uint32_t *>((is_v ? A.lo_v : A.lo_k) + lslot * (kHeadDim * LO_BITS / 8) +
+    uint32_t *codes = reinterpret_cast<uint32_t *>(lane_pick(is_v, A.lo_v, A.lo_k) + lslot * (kHeadDim * LO_BITS / 8) +
                                                    part * (32 * LO_BITS / 8));
 #pragma unroll
     for (int i = 0; i < LO_BITS; ++i) codes[i] = w[i];
   }
   if ((part % (A.group / 32)) == 0)
-    (is_v ? A.lo_vp : A.lo_kp)[lslot * ng + (part * 32) / A.group] = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
+    lane_pick(is_v, A.lo_vp, A.lo_kp)[lslot * ng + (part * 32) / A.group] = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
 }
 
 template <int HI_BITS, int LO_BITS>
@@ -216,8 +216,8 @@ __device__ inline void demote_row(const SelArgs &A, int h, int slot, int64_t lsl
   const int ng = kHeadDim / A.group;
   const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
   const int is_v = threadIdx.x >> 2, part = threadIdx.x & 3;
-  const uint8_t *rows = (is_v ? A.hi_v : A.hi_k) + (int64_t)h * A.cap_hi * hrow;
-  const uint32_t *pars = HI_BITS == 16 ? nullptr : (is_v ? A.hi_vp : A.hi_kp) + (int64_t)h * A.cap_hi * ng;
+  const uint8_t *rows = lane_pick(is_v, A.hi_v, A.hi_k) + (int64_t)h * A.cap_hi * hrow;
+  const uint32_t *pars = HI_BITS == 16 ? nullptr : lane_pick(is_v, A.hi_vp, A.hi_kp) + (int64_t)h * A.cap_hi * ng;
   float x[32];
   load_hi_segment<HI_BITS>(A, rows, pars, slot, part, x);
   store_lo_segment<LO_BITS>(A, h, lslot, is_v, part, x);
@@ -246,11 +246,11 @@ __device__ inline SlotData<HI_BITS> load_slot(const SelArgs &A, int h, int src) 
   const int ng = kHeadDim / A.group;
   SlotData<HI_BITS> d{};
   if (threadIdx.x < 2 * chunks) {
-    const uint8_t *base = (threadIdx.x < chunks ? A.hi_k : A.hi_v) + (int64_t)h * A.cap_hi * hrow;
+    const uint8_t *base = lane_pick(threadIdx.x < chunks, A.hi_k, A.hi_v) + (int64_t)h * A.cap_hi * hrow;
     d.piece = reinterpret_cast<const uint4 *>(base + (int64_t)src * hrow)[threadIdx.x % chunks];
   }
   if (HI_BITS == 8 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
-    const uint32_t *pp = threadIdx.x - 64 < ng ? A.hi_kp : A.hi_vp;
+    const uint32_t *pp = lane_pick(threadIdx.x - 64 < (unsigned)ng, A.hi_kp, A.hi_vp);
     d.par = pp[((int64_t)h * A.cap_hi + src) * ng + (threadIdx.x - 64) % ng];
   }
   if (threadIdx.x == 0) {
@@ -266,11 +266,11 @@ __device__ inline void store_slot(const SelArgs &A, int h, int dst, const SlotDa
   constexpr int chunks = hrow / 16;
   const int ng = kHeadDim / A.group;
   if (threadIdx.x < 2 * chunks) {
-    uint8_t *base = (threadIdx.x < chunks ? A.hi_k : A.hi_v) + (int64_t)h * A.cap_hi * hrow;
+    uint8_t *base = lane_pick(threadIdx.x < chunks, A.hi_k, A.hi_v) + (int64_t)h * A.cap_hi * hrow;
     reinterpret_cast<uint4 *>(base + (int64_t)dst * hrow)[threadIdx.x % chunks] = d.piece;
   }
   if (HI_BITS == 8 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
-    uint32_t *pp = threadIdx.x - 64 < ng ? A.hi_kp : A.hi_vp;
+    uint32_t *pp = lane_pick(threadIdx.x - 64 < (unsigned)ng, A.hi_kp, A.hi_vp);
     pp[((int64_t)h * A.cap_hi + dst) * ng + (threadIdx.x - 64) % ng] = d.par;
   }
   if (threadIdx.x == 0) {
@@ -325,7 +325,7 @@ __device__ inline void select_scan(const SelArgs &A, int h, int from, int n, int
 // `set_n` (n_hi in memory does not yet count an appended token) n_hi is
 // written even when no token leaves.
 template <int HI_BITS, int LO_BITS>
-__device__ void select_finish(const SelArgs &A, int h, int n, int n_lo0, const SelScan &sc,
+__device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, int h, int n, int n_lo0, const SelScan &sc,
                               const SlotData<HI_BITS> &last, bool set_n = false) {
   __shared__ int s_tmp_i[kSel / 64];
   __shared__ uint64_t s_tmp_u[kSel / 64];
@@ -381,8 +381,8 @@ __device__ void select_finish(const SelArgs &A, int h, int n, int n_lo0, const S
   for (int r = threadIdx.x >> 2; r < 2 * n_dem; r += kSel / 4) {
     const int d = r >> 1, is_v = r & 1, part = threadIdx.x & 3;
     const int slot = dem_list[d];
-    const uint8_t *rows = (is_v ? A.hi_v : A.hi_k) + (int64_t)h * A.cap_hi * hrow;
-    const uint32_t *pars = HI_BITS == 16 ? nullptr : (is_v ? A.hi_vp : A.hi_kp) + (int64_t)h * A.cap_hi * ng;
+    const uint8_t *rows = lane_pick(is_v, A.hi_v, A.hi_k) + (int64_t)h * A.cap_hi * hrow;
+    const uint32_t *pars = HI_BITS == 16 ? nullptr : lane_pick(is_v, A.hi_vp, A.hi_kp) + (int64_t)h * A.cap_hi * ng;
     float x[32];
     load_hi_segment<HI_BITS>(A, rows, pars, slot, part, x);
     const int64_t lslot = (int64_t)h * A.cap_lo + n_lo0 + d;
@@ -427,7 +427,7 @@ __device__ void select_finish(const SelArgs &A, int h, int n, int n_lo0, const S
 
 // Re-rank and demote for head h; the whole block (kSel threads) takes part.
 template <int HI_BITS, int LO_BITS>
-__device__ void select_head(const SelArgs &A, int h) {
+__device__ __attribute__((always_inline)) void select_head(const SelArgs &A, int h) {
   const int n_mem = __builtin_amdgcn_readfirstlane(A.n_hi[h]);
   const int n = n_mem + (A.pending && n_mem < A.cap_hi ? 1 : 0);
   const int n_lo0 = __builtin_amdgcn_readfirstlane(A.n_lo[h]);
