@@ -133,18 +133,6 @@ __device__ inline uint32_t encode(float x, const GroupParams &p, int bits) {
   return (uint32_t)t;
 }
 
-// ---------------------------------------------------------------------------
-// Retained-pool 2-bit value codes for GQA: tiles of 32 slots, quad-major.
-// A slot's LSB-first packed 2-bit row has 32 bytes; byte q holds channels
-// 4q..4q+3.  In a tiled value array that byte of slot s sits at (s / 32) * 1024 + 32 * q + (s % 32): the same channel quad
-// of 32 consecutive slots is contiguous, the operand shape the decode
-// attention's matrix cores read (tokens along the reduction).  Every byte
-// belongs to one slot, so slots are written independently.
-// ---------------------------------------------------------------------------
-// The tiled value layout is used where the matrix cores read it: 2-bit
-// retained pools shared by two or more query heads (GQA).  With one query
-// head per KV head the values stay token-major (the vector path reads a
-// token's row per lane).
 // c ? a : b for wave-uniform pointers (argument fields) and a per-lane
 // condition, selected as values: a select between two fields of an argument
 // struct can otherwise become a per-lane indexed load from the struct, which
@@ -159,6 +147,18 @@ __device__ inline T *lane_pick(bool c, T *a, T *b) {
   return reinterpret_cast<T *>(c ? fa : fb);
 }
 
+// ---------------------------------------------------------------------------
+// Retained-pool 2-bit value codes for GQA: tiles of 32 slots, quad-major.
+// A slot's LSB-first packed 2-bit row has 32 bytes; byte q holds channels
+// 4q..4q+3.  In a tiled value array that byte of slot s sits at (s / 32) * 1024 + 32 * q + (s % 32): the same channel quad
+// of 32 consecutive slots is contiguous, the operand shape the decode
+// attention's matrix cores read (tokens along the reduction).  Every byte
+// belongs to one slot, so slots are written independently.
+// ---------------------------------------------------------------------------
+// The tiled value layout is used where the matrix cores read it: 2-bit
+// retained pools shared by two or more query heads (GQA).  With one query
+// head per KV head the values stay token-major (the vector path reads a
+// token's row per lane).
 __host__ __device__ inline bool int2_values_tiled(int lo_bits, int q_heads, int kv_heads) {
   return lo_bits == 2 && q_heads >= 2 * kv_heads;
 }
