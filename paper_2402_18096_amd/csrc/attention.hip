@@ -601,9 +601,9 @@ __host__ __device__ constexpr int tau8(int e) { return (e & 4) | ((e & 1) << 1) 
 // LDS weight staging: [group][value tile][row 0..15][lane group][element]
 // halves; rows past 2G stay zero, so every lane reads its operand.
 __device__ inline int w_index(int gamma, int vt, int row, int g, int e) {
-  return (((gamma * 2 + vt) * 16 + row) * 4 + g) * 8 + e;
+  return (((gamma * kVT + vt) * 16 + row) * 4 + g) * 8 + e;
 }
-constexpr int kWLds = 4 * 2 * 16 * 4 * 8;  // halves (8 KiB)
+constexpr int kWLds = 4 * kVT * 16 * 4 * 8;  // halves (4 KiB per value tile)
 
 template <int G, bool SPLITQ, int NG>
 __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chunk, float *s_lds, _Float16 *w_lds) {
