@@ -48,10 +48,7 @@ __device__ inline GroupParams quantize_words(const float x[32], int group, uint3
     mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   }
   GroupParams p = group_params(mn, mx, BITS);
-#pragma unroll
-  for (int i = 0; i < BITS; ++i) w[i] = 0u;
-#pragma unroll
-  for (int c = 0; c < 32; ++c) w[(c * BITS) / 32] |= encode(x[c], p, BITS) << ((c * BITS) % 32);
+  encode32<BITS>(x, p, w);
   return p;
 }
 

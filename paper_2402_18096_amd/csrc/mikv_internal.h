@@ -133,6 +133,37 @@ __device__ inline uint32_t encode(float x, const GroupParams &p, int bits) {
   return (uint32_t)t;
 }
 
+// encode() of the 32 values of one lane's segment, packed LSB-first into
+// w[BITS], without a divide per value: the quotient (x - beta) / alpha is
+// estimated as (x - beta) * fl(1 / alpha), within 1.5 ulp of the correctly
+// rounded quotient.  The rounded code can only differ where a half-integer
+// lies between the two, so where an estimate is within 2^-20 (relative) of
+// a half-integer the wave recomputes its quotients with the true divide;
+// the codes are then those of encode() bit for bit.
+template <int BITS>
+__device__ inline void encode32(const float x[32], const GroupParams &p, uint32_t w[BITS]) {
+  const float top = (float)((1 << BITS) - 1);
+  const bool zero = p.a == 0.0f;
+  const float ra = zero ? 0.0f : 1.0f / p.a;
+  float q[32];
+  bool near = false;
+#pragma unroll
+  for (int c = 0; c < 32; ++c) {
+    q[c] = (x[c] - p.b) * ra;
+    const float f = q[c] - floorf(q[c]);
+    near = near || fabsf(f - 0.5f) <= fmaxf(fabsf(q[c]), 1.0f) * 0x1p-20f;
+  }
+  if (__ballot(near)) {
+#pragma unroll
+    for (int c = 0; c < 32; ++c) q[c] = zero ? 0.0f : (x[c] - p.b) / p.a;
+  }
+#pragma unroll
+  for (int i = 0; i < BITS; ++i) w[i] = 0u;
+#pragma unroll
+  for (int c = 0; c < 32; ++c)
+    w[(c * BITS) / 32] |= (uint32_t)fminf(fmaxf(rintf(q[c]), 0.0f), top) << ((c * BITS) % 32);
+}
+
 // c ? a : b for wave-uniform pointers (argument fields) and a per-lane
 // condition, selected as values: a select between two fields of an argument
 // struct can otherwise become a per-lane indexed load from the struct, which

@@ -13,6 +13,7 @@ import torch
 import oracle
 from paper_2402_18096_amd import mikv, workloads
 from tests.parity import Lockstep, SampledLockstep, compare_state, np16
+from tests.quant_inputs import tie_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -24,7 +25,7 @@ def _dev():
 
 # -- raw quantizer ----------------------------------------------------------------
 
-def _adversarial_rows(rng, rows):
+def _adversarial_rows(rng, rows, bits, group):
     x = rng.standard_normal((rows, 128)).astype(np.float32) * 2
     x[0::7] += 1000.3                          # offset-dominated groups (clamp)
     x[1::7] *= 1e-6                            # fp16-subnormal alpha and beta
@@ -32,6 +33,7 @@ def _adversarial_rows(rng, rows):
     x[3::7, :64] = 0.7                         # degenerate groups
     x[4::7] *= 500                             # large magnitudes
     x[5::7] = rng.integers(0, 256, (len(x[5::7]), 128))  # integer-valued
+    x[6::7] = tie_rows(rng, len(x[6::7]), bits, group)   # exact quotient ties
     return x.astype(np.float16)
 
 
@@ -42,7 +44,7 @@ def test_quantize_rows_bit_exact(bits, group, balanced):
     dev = _dev()
     rng = np.random.default_rng(bits * 1000 + group + balanced)
     rows = 4099
-    x = _adversarial_rows(rng, rows)
+    x = _adversarial_rows(rng, rows, bits, group)
     bal = None
     rpb = 64
     if balanced:

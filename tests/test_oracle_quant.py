@@ -180,3 +180,25 @@ def test_memory_table_head_shapes():
     assert round(gb(32, 8), 2) == 8.59
     assert round(gb(40, 40), 2) == 53.69
     assert round(gb(32, 32) * 0.25, 2) == 8.59 and round(gb(32, 32) * 0.2, 2) == 6.87
+
+
+@pytest.mark.parametrize("bits", [2, 4, 8])
+def test_exact_quotient_ties_round_half_even(bits):
+    """Eq. 1 on groups whose quotients (x - beta) / alpha are exact
+    half-integers or one fp16 ulp from them: every code is the quotient taken
+    in exact rational arithmetic, rounded half to even and clamped."""
+    from fractions import Fraction
+    from tests.quant_inputs import tie_rows
+    rng = np.random.default_rng(100 + bits)
+    x = tie_rows(rng, 24, bits, 32)
+    c, a, b = oracle.quantize(x.astype(np.float32), bits, 32)
+    al = a.view(np.float16).astype(np.float64)
+    be = b.view(np.float16).astype(np.float64)
+    top = (1 << bits) - 1
+    ties = 0
+    for r in range(x.shape[0]):
+        for j in range(128):
+            q = (Fraction(float(x[r, j])) - Fraction(be[r, j // 32])) / Fraction(al[r, j // 32])
+            ties += q.denominator == 2
+            assert int(c[r, j]) == min(max(round(q), 0), top), (r, j, q)
+    assert ties > x.size // 3
