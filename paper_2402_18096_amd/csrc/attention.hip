@@ -1277,6 +1277,13 @@ void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi, int tiles_lo
 // row).  Block (h, 1) merges the output; blocks (h, 2..) handle the
 // retained-pool tiles.  Heads run along x, so every head's re-rank block is
 // dispatched before any tile block.  No block waits on another.
+#ifndef MIKV_LO_TILES
+#define MIKV_LO_TILES 8
+#endif
+// Retained-pool probability tiles per finalize block (a tile per query head
+// of the group costs the same registers as kLoTiles tiles of one head).
+__host__ __device__ constexpr int lo_tiles_per_block(int G) { return MIKV_LO_TILES / G > 1 ? MIKV_LO_TILES / G : 1; }
+
 template <int G, int HI, int LO>
 __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int tiles_hi, int tiles_lo, SelArgs S) {
   static_assert(kSel == kBlock && kSelItems * kBlock == 2 * kProbTile, "select items = two probability tiles");
@@ -1291,11 +1298,18 @@ __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int
     return;
   }
   if (c > 1) {
-    const bool has_tile = c - 2 < tiles_lo;
-    const ProbTile<G> T = prob_tile_load<G>(A, h, qh0, false, c - 2, has_tile, false);
+    // kLoTiles retained-pool tiles per block, all loaded before the
+    // statistics: fewer, longer blocks (one round of blocks per step)
+    constexpr int KT = lo_tiles_per_block(G);
+    const int t0 = (c - 2) * KT;
+    ProbTile<G> T[KT];
+#pragma unroll
+    for (int k = 0; k < KT; ++k) T[k] = prob_tile_load<G>(A, h, qh0, false, t0 + k, t0 + k < tiles_lo, false);
     float M[G], inv[G];
     head_stats<G>(A, qh0, nc, M, inv);
-    if (has_tile) prob_tile_store<G>(A, h, qh0, false, false, T, M, inv);
+#pragma unroll
+    for (int k = 0; k < KT; ++k)
+      if (t0 + k < tiles_lo) prob_tile_store<G>(A, h, qh0, false, false, T[k], M, inv);
     return;
   }
   // Everything the re-rank reads besides the new scores is loaded together
@@ -1557,7 +1571,8 @@ int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int tiles_hi = (span_hi + kProbTile - 1) / kProbTile;  // probabilities accumulated
   const int tiles_lo = A.probs_lo ? (span_lo + kProbTile - 1) / kProbTile : 0;
-  dim3 grid(n_heads_of(c), 2 + tiles_lo);  // y = 0: importance pool and re-rank, 1: output
+  const int kt = lo_tiles_per_block(group_size_of(c));
+  dim3 grid(n_heads_of(c), 2 + (tiles_lo + kt - 1) / kt);  // y = 0: importance pool and re-rank, 1: output
   const int G = group_size_of(c);
   switch (c->hi_bits * 100 + c->lo_bits) {
     case 1602: launch_finalize_select<16, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
