@@ -15,7 +15,9 @@ before the timed region starts.  Prints ONE JSON line on stdout:
   roofline   the attention partial kernel (the dominant one): its algorithmic
              bytes per launch (the packed K/V bytes) / its mean duration from
              HIP events recorded on its stream, against 8 TB/s;
-  cpu_baseline  the CPU oracle timed on a bounded sample of the same workload.
+  cpu_baseline  the CPU oracle timed on a bounded sample of the same workload;
+  mall       untimed diagnostic: event-bracketed whole steps with warm caches
+             and with the 256 MB last-level cache flushed before each step.
 
 Only one GPU is used; --gpus above 1 exits with an error.
 """
@@ -171,6 +173,10 @@ def main():
     ap.add_argument("--event-every", type=int, default=8, metavar="K",
                     help="bracket the attention partial kernel with events on every K-th timed step (each event "
                          "costs a few microseconds of GPU time; default 8)")
+    ap.add_argument("--mall-steps", type=int, default=16,
+                    help="untimed steps after the phase pass, each bracketed by two events: this many with the "
+                         "caches as the previous step left them (warm), then this many each preceded by a "
+                         "1 GiB read that evicts the 256 MB last-level cache (cold)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
                     help="instead of the bench: time a plain device-to-device copy of MB megabytes")
     args = ap.parse_args()
@@ -192,7 +198,7 @@ def main():
         cur = getattr(wl, key)
         wl = wl.with_(**{key: type(cur)(val) if not isinstance(cur, bool) else val in ("1", "true", "True")})
     dev = torch.device("cuda:0")
-    n_total = args.warmup + args.steps + args.phase_steps
+    n_total = args.warmup + args.steps + args.phase_steps + 2 * args.mall_steps
     t_setup = time.perf_counter()
     dec = mikv.MikvDecoder(wl, max_len=wl.context + n_total, device=dev, fused=bool(args.fused))
     k, v = workloads.prefill_kv(wl, dev)
@@ -256,6 +262,39 @@ def main():
     dur = {p: [ph_ev[i][j].elapsed_time(ph_ev[i][j + 1]) for i in range(args.phase_steps)]
            for j, p in enumerate(phases)}
 
+    # Diagnostics, untimed: whole steps bracketed by events, warm, then cold
+    # (the last-level cache and L2 flushed by reading 1 GiB before each
+    # step, outside the bracket; a read leaves no dirty lines behind).
+    mall = None
+    if args.mall_steps > 0:
+        flush = torch.zeros(1 << 28, dtype=torch.float32, device=dev)
+        mb, ln, nh = [], dec.length, int(dec.cache.n_hi[0].item())
+        for _ in range(2 * args.mall_steps):
+            ln, n_attn, nh = track_counts(dec, nh, ln)
+            mb.append(dec.cache.packed_bytes(ln, n_attn))
+        res = {}
+        base = args.warmup + args.steps + args.phase_steps
+        for j, kind in enumerate(("warm", "cold")):
+            evs = [fresh_events(2) for _ in range(args.mall_steps)]
+            torch.cuda.synchronize()
+            for i in range(args.mall_steps):
+                t = base + j * args.mall_steps + i
+                if kind == "cold":
+                    flush.sum()  # reads only: no dirty lines left to write back
+                evs[i][0].record()
+                dec.step_native(q[t], kn[t], vn[t])
+                evs[i][1].record()
+            torch.cuda.synchronize()
+            us = sorted(e[0].elapsed_time(e[1]) * 1e3 for e in evs)
+            nb = mb[j * args.mall_steps:(j + 1) * args.mall_steps]
+            res[kind] = {"step_us_median": round(us[len(us) // 2], 2), "step_us_mean": round(sum(us) / len(us), 2),
+                         "effective_GBps_median": round(sum(nb) / len(nb) / (us[len(us) // 2] * 1e-6) / 1e9, 1)}
+        del flush
+        mall = {**res, "steps_each": args.mall_steps, "flush": "1 GiB fp32 read (sum) before each cold step",
+                "note": "each step bracketed by two events on the stream (adds about empty_event_bracket_us)"}
+        log(f"[bench] whole step (event-bracketed): warm median {res['warm']['step_us_median']} us, "
+            f"cold median {res['cold']['step_us_median']} us")
+
     total_bytes = sum(step_bytes)
     value = total_bytes / elapsed / 1e9
     ms = elapsed / args.steps * 1e3
@@ -318,6 +357,7 @@ def main():
         "packed_bytes_per_step": int(mean_bytes),
         "phase_us": {p: round(mean(dur[p]) * 1e3, 2) for p in phases},
         "roofline": roofline,
+        "mall": mall,
         "cpu_baseline": cpu,
     }
     if args.override:
