@@ -78,7 +78,7 @@ def cpu_baseline(wl, steps_inputs, budget_s: float):
     orc.prefill(kk, vv, sc[heads], oracle.heavy_budget(T, wl.ratio_num, wl.ratio_den, wl.window,
                                                        wl.window_in_ratio), wl.window, bal)
     qh = [h * G + i for h in heads for i in range(G)]
-    tb = lambda bits: 4 * 128 if bits == 16 else 2 * (128 * bits // 8 + 4 * (128 // wl.group))
+    tb = lambda bits: 0 if bits == 0 else 4 * 128 if bits == 16 else 2 * (128 * bits // 8 + 4 * (128 // wl.group))
     done, nbytes, t0 = 0, 0, time.perf_counter()
     while done < n_steps and time.perf_counter() - t0 < budget_s:
         L = orc.length + 1

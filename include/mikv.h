@@ -78,6 +78,13 @@ enum mikv_attention_flags {
  *   lo_k, lo_v   uint8 packed codes [NH, cap_lo, 128 * lo_bits / 8];
  *   lo_kp, lo_vp fp16 (alpha, beta) pairs [NH, cap_lo, 128/group, 2];
  *   lo_pos [NH, cap_lo] int32; n_lo [NH] int32.
+ * lo_bits == 0 selects the paper's eviction baseline (H2O, the cache with
+ *   0-bit retained tokens of Section 4 / Table 1): there is no retained
+ *   pool, a token left out of the importance pool at prefill or demoted by
+ *   the re-rank is dropped, and attention covers the importance pool only.
+ *   lo_k, lo_v, lo_kp, lo_vp and lo_pos are then unused (may be NULL),
+ *   cap_lo is ignored, n_lo (still required) stays as the caller set it,
+ *   probs_lo is not written, and map 0 means "evicted".
  * Codes: Eq. 1 per token and per group of `group` contiguous channels, packed
  * least-significant-bits first (channel c at byte c*N/8, bit (c*N)%8).
  * Keys are stored balanced (Eq. 3) when a balancer is in use.
@@ -94,9 +101,9 @@ typedef struct mikv_cache {
   int32_t head_dim;   /* 128 */
   int32_t group;      /* quantization group size: 32, 64 or 128 channels */
   int32_t hi_bits;    /* 16 (fp16) or 8 (INT8) */
-  int32_t lo_bits;    /* 2, 4 or 8 */
+  int32_t lo_bits;    /* 2, 4 or 8; 0 = evict instead of retaining (see above) */
   int32_t cap_hi;     /* importance-pool slots per head */
-  int32_t cap_lo;     /* retained-pool slots per head */
+  int32_t cap_lo;     /* retained-pool slots per head (ignored when lo_bits is 0) */
   int32_t max_len;    /* positions per head (length of map rows) */
   void *hi_k, *hi_v;
   uint16_t *hi_kp, *hi_vp;

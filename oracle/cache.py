@@ -18,6 +18,11 @@ Step order (Fig. 3; H2O order -- attend, accumulate, then evict/demote):
      already balanced, so the balancer is not applied again.
 Prefill stores the prompt's tokens after a first selection in which every
 token outside the window is eligible, scored by the supplied initial scores.
+
+``lo_bits = 0`` is the eviction baseline the paper compares against (H2O, a
+retained cache of 0 bits, Section 4 / Table 1): a token outside the
+importance cache is dropped, and attention runs over the importance cache
+alone (its probabilities are 0 at evicted positions).
 """
 from __future__ import annotations
 
@@ -35,7 +40,7 @@ class OracleCache:
 
     def __init__(self, n_heads: int, group_size: int, max_len: int, hi_bits: int, lo_bits: int,
                  group: int, head_dim: int = 128):
-        assert hi_bits in (16, 8) and lo_bits in (2, 4, 8)
+        assert hi_bits in (16, 8) and lo_bits in (0, 2, 4, 8)
         self.n_heads, self.G, self.max_len = n_heads, group_size, max_len
         self.hi_bits, self.lo_bits, self.group, self.d = hi_bits, lo_bits, group, head_dim
         ng = head_dim // group
@@ -65,6 +70,8 @@ class OracleCache:
 
     def _store_lo(self, h, pos, kx, vx):
         n = self.lo_bits
+        if n == 0:  # evicted: nothing is kept
+            return
         self.lk[h, pos], self.lk_a[h, pos], self.lk_b[h, pos] = quantize(kx, n, self.group)
         self.lv[h, pos], self.lv_a[h, pos], self.lv_b[h, pos] = quantize(vx, n, self.group)
 
@@ -88,7 +95,10 @@ class OracleCache:
         k = np.empty((L, self.d), np.float32)
         v = np.empty((L, self.d), np.float32)
         k[hi], v[hi] = self._hi_values(h, pos[hi])
-        k[~hi], v[~hi] = self._lo_values(h, pos[~hi])
+        if self.lo_bits:
+            k[~hi], v[~hi] = self._lo_values(h, pos[~hi])
+        else:  # evicted positions hold nothing
+            k[~hi], v[~hi] = 0.0, 0.0
         return k, v
 
     # -- phases -------------------------------------------------------------
@@ -127,7 +137,13 @@ class OracleCache:
         p = np.empty((self.n_heads, self.G, self.length), np.float32)
         for h in range(self.n_heads):
             k, v = self.values(h)
-            o[h], p[h] = attention(q16[h], k, v, scale, None if balance is None else balance[h])
+            b = None if balance is None else balance[h]
+            if self.lo_bits:
+                o[h], p[h] = attention(q16[h], k, v, scale, b)
+            else:  # eviction: only the importance cache is attended
+                keep = self.is_hi[h, :self.length]
+                p[h] = 0.0
+                o[h], p[h][:, keep] = attention(q16[h], k[keep], v[keep], scale, b)
         return o, p
 
     def accumulate(self, probs):

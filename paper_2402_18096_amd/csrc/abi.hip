@@ -41,16 +41,16 @@ int validate_cache(const mikv_cache *c) {
     return set_error(MIKV_ERR_UNSUPPORTED, "group must be 32, 64 or 128 (got %d)", c->group);
   if (c->hi_bits != 16 && c->hi_bits != 8)
     return set_error(MIKV_ERR_UNSUPPORTED, "hi_bits must be 16 or 8 (got %d)", c->hi_bits);
-  if (c->lo_bits != 2 && c->lo_bits != 4 && c->lo_bits != 8)
-    return set_error(MIKV_ERR_UNSUPPORTED, "lo_bits must be 2, 4 or 8 (got %d)", c->lo_bits);
-  if (c->cap_hi < 1 || c->cap_lo < 1 || c->max_len < 1)
-    return set_error(MIKV_ERR_INVALID_ARG, "cap_hi, cap_lo and max_len must be >= 1");
+  if (c->lo_bits != 0 && c->lo_bits != 2 && c->lo_bits != 4 && c->lo_bits != 8)
+    return set_error(MIKV_ERR_UNSUPPORTED, "lo_bits must be 0, 2, 4 or 8 (got %d)", c->lo_bits);
+  if (c->cap_hi < 1 || (!evicting(c) && c->cap_lo < 1) || c->max_len < 1)
+    return set_error(MIKV_ERR_INVALID_ARG, "cap_hi, cap_lo (unless lo_bits is 0) and max_len must be >= 1");
   if (int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) && c->cap_lo % 32 != 0)
     return set_error(MIKV_ERR_INVALID_ARG,
                      "cap_lo must be a multiple of 32 for a 2-bit retained pool shared by query heads (got %d)",
                      c->cap_lo);
-  if (!c->hi_k || !c->hi_v || !c->hi_pos || !c->hi_acc || !c->n_hi || !c->lo_k || !c->lo_v ||
-      !c->lo_kp || !c->lo_vp || !c->lo_pos || !c->n_lo || !c->status)
+  if (!c->hi_k || !c->hi_v || !c->hi_pos || !c->hi_acc || !c->n_hi || !c->n_lo || !c->status ||
+      (!evicting(c) && (!c->lo_k || !c->lo_v || !c->lo_kp || !c->lo_vp || !c->lo_pos)))
     return set_error(MIKV_ERR_INVALID_ARG, "a required cache pointer is NULL");
   if (c->hi_bits == 8 && (!c->hi_kp || !c->hi_vp))
     return set_error(MIKV_ERR_INVALID_ARG, "hi_kp/hi_vp are required for an INT8 importance pool");

@@ -1386,8 +1386,9 @@ int round_up(int64_t x, int m) { return (int)(((x + m - 1) / m) * m); }
 Plan make_plan(const mikv_cache *c, int length) {
   Plan p;
   const int64_t NH = n_heads_of(c);
-  const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
-  const int64_t bh = token_bytes(c->hi_bits, c->group), bl = token_bytes(c->lo_bits, c->group);
+  // an evicting cache has no retained pool: no chunks for it
+  const int span_hi = std::min(length, c->cap_hi), span_lo = evicting(c) ? 0 : std::min(length, c->cap_lo);
+  const int64_t bh = token_bytes(c->hi_bits, c->group), bl = token_bytes(evicting(c) ? 2 : c->lo_bits, c->group);
   const int64_t total = NH * (span_hi * bh + span_lo * bl);
   // One wave per chunk; up to 96 KiB of packed K/V per chunk (many small work
   // units balance the CUs best), at least 16 KiB so the per-chunk merge
@@ -1401,7 +1402,7 @@ Plan make_plan(const mikv_cache *c, int length) {
   p.chunk_hi = std::min(cmax, std::max(128, round_up(target_hi / bh, 128)));
   p.chunk_lo = std::min(cmax, std::max(128, round_up(target / bl, 128)));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
-  p.nc_lo = std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
+  p.nc_lo = evicting(c) ? 0 : std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
   // every token is in one of the pools, so at least length - cap_hi are in
   // the retained one (only the dispatch order depends on this)
   const int lo_min = std::max(0, std::min(span_lo, length - c->cap_hi));
@@ -1537,7 +1538,7 @@ int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const
   if (k_new) set_append(A, c, length, k_new, v_new, balance);
   dim3 grid((p.nc_hi + p.nc_lo) * n_heads_of(c));
   const int G = group_size_of(c);
-  switch (c->hi_bits * 100 + c->lo_bits) {
+  switch (format_key(c)) {
     case 1602: launch_partial_g<16, 2>(A, G, grid, st); break;
     case 1604: launch_partial_g<16, 4>(A, G, grid, st); break;
     case 1608: launch_partial_g<16, 8>(A, G, grid, st); break;
@@ -1570,11 +1571,11 @@ int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *
   const SelArgs S = make_sel_args(c, length, k_heavy, window, sel_ws);
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int tiles_hi = (span_hi + kProbTile - 1) / kProbTile;  // probabilities accumulated
-  const int tiles_lo = A.probs_lo ? (span_lo + kProbTile - 1) / kProbTile : 0;
+  const int tiles_lo = A.probs_lo && !evicting(c) ? (span_lo + kProbTile - 1) / kProbTile : 0;
   const int kt = lo_tiles_per_block(group_size_of(c));
   dim3 grid(n_heads_of(c), 2 + (tiles_lo + kt - 1) / kt);  // y = 0: importance pool and re-rank, 1: output
   const int G = group_size_of(c);
-  switch (c->hi_bits * 100 + c->lo_bits) {
+  switch (format_key(c)) {
     case 1602: launch_finalize_select<16, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 1604: launch_finalize_select<16, 4>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 1608: launch_finalize_select<16, 8>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
@@ -1610,7 +1611,7 @@ int decode_finalize(const mikv_cache *c, int32_t length, const uint16_t *q, cons
   // accumulated, retained pool when its probabilities are emitted
   const int span_hi = std::min(length, c->cap_hi), span_lo = std::min(length, c->cap_lo);
   const int tiles_hi = (A.scores_hi && (A.probs_hi || A.acc)) ? (span_hi + kProbTile - 1) / kProbTile : 0;
-  const int tiles_lo = A.probs_lo ? (span_lo + kProbTile - 1) / kProbTile : 0;
+  const int tiles_lo = A.probs_lo && !evicting(c) ? (span_lo + kProbTile - 1) / kProbTile : 0;
   dim3 grid(n_heads_of(c), 1 + tiles_hi + tiles_lo);  // y = 0: output
   switch (group_size_of(c)) {
     case 1: hipLaunchKernelGGL(attn_finalize_kernel<1>, grid, dim3(kBlock), 0, st, A, acc, tiles_hi, tiles_lo); break;

@@ -45,6 +45,12 @@ int select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t wi
                 bool appended, hipStream_t st);
 
 inline int group_size_of(const mikv_cache *c) { return c->q_heads / c->kv_heads; }
+// lo_bits == 0: no retained pool; tokens that leave the importance pool are
+// evicted (the 0-bit retained cache, i.e. H2O eviction).
+inline bool evicting(const mikv_cache *c) { return c->lo_bits == 0; }
+// Key of the kernel instantiation for the cache's formats.  An evicting
+// cache runs the 2-bit instantiation with its retained pool empty.
+inline int format_key(const mikv_cache *c) { return c->hi_bits * 100 + (evicting(c) ? 2 : c->lo_bits); }
 inline int n_heads_of(const mikv_cache *c) { return c->batch * c->kv_heads; }
 
 // Bytes of one token (key + value, codes + fp16 params) in a pool of `bits`.

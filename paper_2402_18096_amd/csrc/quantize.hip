@@ -47,6 +47,7 @@ struct Pools {
   int32_t *status;
   int cap_hi, cap_lo, max_len, group;
   int v_tiled;  // 2-bit values in the tiled layout (int2_values_tiled)
+  int evict;    // no retained pool: tokens not placed in the importance pool are dropped
 };
 
 Pools make_pools(const mikv_cache *c) {
@@ -71,6 +72,7 @@ Pools make_pools(const mikv_cache *c) {
   p.max_len = c->max_len;
   p.group = c->group;
   p.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
+  p.evict = evicting(c) ? 1 : 0;
   return p;
 }
 
@@ -176,7 +178,9 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
   if (live) {
     int slot = is_hi ? s_base[0] + r_hi : s_base[1] + r_lo;
     int cap = is_hi ? P.cap_hi : P.cap_lo;
-    if (slot >= cap) {
+    if (!is_hi && P.evict) {
+      slot = -1;  // evicted: stored nowhere (the map says "not in the importance pool")
+    } else if (slot >= cap) {
       atomicOr(P.status, is_hi ? MIKV_DEVERR_HI_FULL : MIKV_DEVERR_LO_FULL);
       slot = -1;
     }
@@ -191,6 +195,8 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
         P.lo_pos[(int64_t)h * P.cap_lo + slot] = pos;
       }
       if (P.map) P.map[(int64_t)h * P.max_len + pos] = (uint8_t)is_hi;
+    } else if (!is_hi && P.evict && P.map) {
+      P.map[(int64_t)h * P.max_len + pos] = 0;
     }
   }
   __syncthreads();
@@ -227,6 +233,9 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
         uint32_t *par = (is_v ? P.hi_vp : P.hi_kp) + ((int64_t)h * P.cap_hi + sl) * ng + (lane4 * 32) / P.group;
         quantize_segment<8>(x, P.group, lane4, dst, par, store);
       }
+    } else if (P.evict) {
+      // evicted token (no retained pool): nothing to store; the four lanes
+      // of the row take this branch together
     } else if (LO_BITS == 2 && is_v && P.v_tiled) {
       // 2-bit values of a GQA cache go to the tiled layout, byte by byte
       uint32_t w[2];
@@ -248,7 +257,7 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
     __syncthreads();
     if (tid == 0) {
       P.n_hi[h] = min(n_hi0 + s_total[0], P.cap_hi);
-      P.n_lo[h] = min(n_lo0 + s_total[1], P.cap_lo);
+      if (!P.evict) P.n_lo[h] = min(n_lo0 + s_total[1], P.cap_lo);
     }
   }
 }
@@ -285,7 +294,7 @@ __global__ void commit_counts_kernel(Pools P, int n_heads, int n, const int32_t 
     tl = n - th;
   }
   P.n_hi[h] = min(P.n_hi[h] + th, P.cap_hi);
-  P.n_lo[h] = min(P.n_lo[h] + tl, P.cap_lo);
+  if (!P.evict) P.n_lo[h] = min(P.n_lo[h] + tl, P.cap_lo);
 }
 
 template <int HI_BITS, int LO_BITS>
@@ -372,8 +381,7 @@ extern "C" int mikv_quantize_kv(const mikv_cache *c, const uint16_t *k, const ui
   }
   hipStream_t st = (hipStream_t)stream;
   int32_t *counts = (int32_t *)workspace;
-  int key = c->hi_bits * 100 + c->lo_bits;
-  switch (key) {
+  switch (format_key(c)) {
     case 1602: launch_place<16, 2>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 1604: launch_place<16, 4>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 1608: launch_place<16, 8>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;

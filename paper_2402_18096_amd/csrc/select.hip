@@ -68,7 +68,7 @@ int select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t wi
   SelArgs A = make_sel_args(c, length, k_heavy, window, ws);
   A.pending = appended ? 1 : 0;
   const int NH = n_heads_of(c);
-  switch (c->hi_bits * 100 + c->lo_bits) {
+  switch (format_key(c)) {
     case 1602: launch_select<16, 2>(A, NH, st); break;
     case 1604: launch_select<16, 4>(A, NH, st); break;
     case 1608: launch_select<16, 8>(A, NH, st); break;

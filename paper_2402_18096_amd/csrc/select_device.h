@@ -136,6 +136,7 @@ struct SelArgs {
   int length, k_heavy, window;
   int v_tiled;  // 2-bit values in the tiled layout (int2_values_tiled)
   int pending;  // n_hi does not yet count the step's appended token (slot n_hi holds it)
+  int evict;    // no retained pool: a token that leaves the importance pool is dropped
 };
 
 // Decode the 32 channels [part*32, part*32+32) of an importance-pool row.
@@ -338,7 +339,7 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
 
   const int n_elig = block_sum_int(sc.cnt, s_tmp_i);
   const int n_dem = n_elig - A.k_heavy;
-  if (n_dem <= 0 || n_lo0 + n_dem > A.cap_lo) {
+  if (n_dem <= 0 || (!A.evict && n_lo0 + n_dem > A.cap_lo)) {
     if (threadIdx.x == 0) {
       if (n_dem > 0) atomicOr(A.status, MIKV_DEVERR_LO_FULL);
       if (set_n) A.n_hi[h] = n;
@@ -354,12 +355,15 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
     __syncthreads();
     const int slot = s_arg[0];
     // the key's low word is the position
-    demote_row<HI_BITS, LO_BITS>(A, h, slot, (int64_t)h * A.cap_lo + n_lo0, (int)(uint32_t)cut);
+    if (!A.evict)
+      demote_row<HI_BITS, LO_BITS>(A, h, slot, (int64_t)h * A.cap_lo + n_lo0, (int)(uint32_t)cut);
+    else if (threadIdx.x == 0 && A.map)
+      A.map[(int64_t)h * A.max_len + (int)(uint32_t)cut] = 0;
     __syncthreads();
     if (slot != n - 1) store_slot<HI_BITS>(A, h, slot, last);
     if (threadIdx.x == 0) {
       A.n_hi[h] = n - 1;
-      A.n_lo[h] = n_lo0 + 1;
+      if (!A.evict) A.n_lo[h] = n_lo0 + 1;
     }
     return;
   }
@@ -378,7 +382,7 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
   // re-quantize the demoted tokens into the retained pool (4 lanes per row)
   const int ng = kHeadDim / A.group;
   const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
-  for (int r = threadIdx.x >> 2; r < 2 * n_dem; r += kSel / 4) {
+  for (int r = threadIdx.x >> 2; r < (A.evict ? 0 : 2 * n_dem); r += kSel / 4) {
     const int d = r >> 1, is_v = r & 1, part = threadIdx.x & 3;
     const int slot = dem_list[d];
     const uint8_t *rows = lane_pick(is_v, A.hi_v, A.hi_k) + (int64_t)h * A.cap_hi * hrow;
@@ -392,6 +396,9 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
       A.lo_pos[lslot] = p;
       if (A.map) A.map[(int64_t)h * A.max_len + p] = 0;
     }
+  }
+  if (A.evict && A.map) {
+    for (int d = threadIdx.x; d < n_dem; d += kSel) A.map[(int64_t)h * A.max_len + pos[dem_list[d]]] = 0;
   }
   __syncthreads();
 
@@ -421,7 +428,7 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
   __syncthreads();
   if (threadIdx.x == 0) {
     A.n_hi[h] = n_new;
-    A.n_lo[h] = n_lo0 + n_dem;
+    if (!A.evict) A.n_lo[h] = n_lo0 + n_dem;
   }
 }
 
@@ -467,6 +474,7 @@ inline SelArgs make_sel_args(const mikv_cache *c, int length, int k_heavy, int w
   A.window = window;
   A.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
   A.pending = 0;
+  A.evict = evicting(c) ? 1 : 0;
   return A;
 }
 

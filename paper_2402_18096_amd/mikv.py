@@ -122,11 +122,15 @@ class MikvCache:
     """Device buffers of one mixed-precision cache (see ``struct mikv_cache``).
 
     A 2-bit retained pool shared by several query heads keeps its value codes
-    in tiles of 32 slots, so its capacity is rounded up to a multiple of 32."""
+    in tiles of 32 slots, so its capacity is rounded up to a multiple of 32.
+    ``lo_bits=0`` is the eviction baseline: no retained pool is allocated
+    (capacity 0) and tokens that leave the importance pool are dropped."""
 
     def __init__(self, batch: int, q_heads: int, kv_heads: int, group: int, hi_bits: int, lo_bits: int,
                  cap_hi: int, cap_lo: int, max_len: int, device="cuda", with_map: bool = True):
         self.values_tiled = lo_bits == 2 and q_heads >= 2 * kv_heads
+        if lo_bits == 0:
+            cap_lo = 0
         if self.values_tiled:
             cap_lo = (cap_lo + 31) // 32 * 32
         self.batch, self.q_heads, self.kv_heads = batch, q_heads, kv_heads
@@ -168,6 +172,8 @@ class MikvCache:
         """Packed K/V bytes of the cache (codes + fp16 alpha/beta + fp16 values)
         when every head holds `length` tokens, `n_hi` of them high precision."""
         def tb(bits):
+            if bits == 0:  # evicted tokens are not stored
+                return 0
             return 4 * HEAD_DIM if bits == 16 else 2 * (HEAD_DIM * bits // 8 + 4 * (HEAD_DIM // self.group))
         return self.n_heads * (n_hi * tb(self.hi_bits) + (length - n_hi) * tb(self.lo_bits))
 

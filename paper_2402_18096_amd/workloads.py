@@ -46,7 +46,7 @@ class Workload:
     context: int          # tokens in the cache before the first decode step
     steps: int            # decode steps the workload runs
     hi_bits: int          # 16 = fp16 importance cache, 8 = INT8
-    lo_bits: int          # retained-cache precision (2 or 4)
+    lo_bits: int          # retained-cache precision (2 or 4; 0 = evict, the H2O baseline)
     group: int            # quantization group size (channels)
     ratio_num: int
     ratio_den: int

@@ -78,10 +78,14 @@ def compare_state(c: mikv.MikvCache, orc: oracle.OracleCache, heads=None, tag=""
         nh, nl = int(s["n_hi"][gh]), int(s["n_lo"][gh])
         hp = s["hi_pos"][gh, :nh]
         lp = s["lo_pos"][gh, :nl]
-        assert nh + nl == L, f"{tag} head {gh}: {nh}+{nl} tokens, expected {L}"
         pos_hi = np.zeros(L, bool)
         pos_hi[hp] = True
-        assert len(set(hp.tolist()) | set(lp.tolist())) == L, f"{tag} head {gh}: positions not a partition"
+        if orc.lo_bits:
+            assert nh + nl == L, f"{tag} head {gh}: {nh}+{nl} tokens, expected {L}"
+            assert len(set(hp.tolist()) | set(lp.tolist())) == L, f"{tag} head {gh}: positions not a partition"
+        else:  # eviction: nothing is retained, every importance-pool position distinct
+            assert nl == 0, f"{tag} head {gh}: {nl} retained tokens in an evicting cache"
+            assert len(set(hp.tolist())) == nh, f"{tag} head {gh}: repeated positions"
         np.testing.assert_array_equal(pos_hi, orc.is_hi[oh, :L], err_msg=f"{tag} head {gh}: precision map")
         if s["map"] is not None:
             np.testing.assert_array_equal(s["map"][gh, :L].astype(bool), pos_hi, err_msg=f"{tag} head {gh}: map")
@@ -97,6 +101,8 @@ def compare_state(c: mikv.MikvCache, orc: oracle.OracleCache, heads=None, tag=""
                                       err_msg=f"{tag} head {gh}: importance scores")
         # retained pool: packed codes and fp16 scale/zero
         bits = orc.lo_bits
+        if bits == 0:
+            continue
         np.testing.assert_array_equal(s["lk"][gh, :nl], oracle.pack(orc.lk[oh, lp], bits), err_msg=f"{tag} lo K codes")
         np.testing.assert_array_equal(s["lv"][gh, :nl], oracle.pack(orc.lv[oh, lp], bits), err_msg=f"{tag} lo V codes")
         np.testing.assert_array_equal(s["lkp"][gh, :nl, :, 0], orc.lk_a[oh, lp], err_msg=f"{tag} lo K alpha")
@@ -110,7 +116,8 @@ def probs_by_position(c: mikv.MikvCache, probs_hi, probs_lo, n_hi, n_lo, hi_pos,
     G = c.q_heads // c.kv_heads
     ph = probs_hi.cpu().numpy().reshape(c.n_heads, G, c.cap_hi)
     pl = probs_lo.cpu().numpy().reshape(c.n_heads, G, c.cap_lo)
-    out = np.full((c.n_heads, G, L), np.nan, np.float32)
+    # an evicting cache gives evicted positions probability 0
+    out = np.full((c.n_heads, G, L), np.nan if c.lo_bits else 0.0, np.float32)
     for h in range(c.n_heads):
         out[h][:, hi_pos[h, :n_hi[h]]] = ph[h, :, :n_hi[h]]
         out[h][:, lo_pos[h, :n_lo[h]]] = pl[h, :, :n_lo[h]]
@@ -246,7 +253,7 @@ class SampledLockstep:
             hi_pos_att[i, n_hi0[i]] = L - 1
         ph = self._rows(self.dec.probs_hi, G)
         pl = self._rows(self.dec.probs_lo, G)
-        p_gpu = np.full((S, G, L), np.nan, np.float32)
+        p_gpu = np.full((S, G, L), np.nan if wl.lo_bits else 0.0, np.float32)
         for i in range(S):
             p_gpu[i][:, hi_pos_att[i, :n_hi_att[i]]] = ph[i, :, :n_hi_att[i]]
             p_gpu[i][:, lo_pos0[i, :n_lo0[i]]] = pl[i, :, :n_lo0[i]]

@@ -195,6 +195,48 @@ def test_lockstep_single_pool(ratio):
         run.step(t)
 
 
+@pytest.mark.parametrize("name", ["long_context", "llama2_13b", "mistral_7b"])
+@pytest.mark.parametrize("fused", [False, True])
+def test_lockstep_eviction(name, fused):
+    """The eviction baseline (lo_bits 0, H2O): no retained pool, attention
+    over the importance pool only, demoted tokens dropped -- fp16 and
+    balanced INT8 importance pools, MHA and GQA."""
+    _dev()
+    wl = workloads.small_workload(name, **SMALL[name], lo_bits=0)
+    run = Lockstep(wl, 4, fused=fused)
+    run.prefill()
+    for t in range(4):
+        run.step(t)
+
+
+def test_lockstep_eviction_many_demotions():
+    """Several evictions per head and step (the radix-select path)."""
+    _dev()
+    wl = workloads.small_workload("long_context", batch=1, q_heads=2, kv_heads=2, context=2000, ratio_num=1,
+                                  ratio_den=4, lo_bits=0)
+    run = Lockstep(wl, 2)
+    run.prefill()
+    run.step(0)
+    run.wl = wl.with_(ratio_den=6)
+    run.dec.wl = run.wl
+    run.step(1)
+
+
+def test_full_size_eviction_sampled_heads():
+    """The eviction baseline at the long_context size in the benchmark's
+    launch configuration, the oracle following three heads."""
+    _dev()
+    wl = workloads.WORKLOADS["long_context"].with_(lo_bits=0)
+    NH = wl.n_heads
+    print(f"[full-size eviction] long_context: {NH} heads, context {wl.context}, 2 steps", flush=True)
+    run = SampledLockstep(wl, 2, heads=[0, NH // 2 + 1, NH - 1])
+    run.prefill()
+    for t in range(2):
+        run.step(t)
+    del run
+    torch.cuda.empty_cache()
+
+
 def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
     dev = _dev()
     c = mikv.MikvCache(1, 2, 2, 32, 16, 2, cap_hi=4, cap_lo=32, max_len=64, device=dev)

@@ -230,6 +230,42 @@ def test_uniform_rtn_special_case():
     np.testing.assert_array_equal(c.lk_a[:, 64], a)
 
 
+def test_eviction_baseline_attends_to_the_kept_tokens_only():
+    """lo_bits 0, the eviction baseline the paper compares against (H2O: a
+    retained cache of 0 bits).  Prefill keeps exactly the window and the
+    k_heavy best-scored tokens outside it (brute-force ranking by score, then
+    newer position); each step's attention is textbook attention (torch SDPA,
+    fp64) over the fp16 keys and values of the kept tokens alone, evicted
+    positions get probability 0, and an evicted token never comes back."""
+    wl = workloads.WORKLOADS["tiny"].with_(batch=1, q_heads=3, kv_heads=3)
+    T, steps, W, kh = 64, 4, 8, 12
+    wl, k, v, sc, q, kn, vn = _tiny_inputs(wl, T, steps, seed=5)
+    H = wl.n_heads
+    c = oracle.OracleCache(H, 1, T + steps, 16, 0, 32)
+    c.prefill(k, v, sc, k_heavy=kh, window=W)
+    for h in range(H):
+        order = sorted(range(T - W), key=lambda j: (-float(sc[h, j]), -j))
+        assert set(np.nonzero(c.is_hi[h, :T])[0].tolist()) == set(order[:kh]) | set(range(T - W, T))
+    K_all = np.concatenate([k, kn[:steps, 0].numpy().transpose(1, 0, 2)], axis=1).astype(np.float64)
+    V_all = np.concatenate([v, vn[:steps, 0].numpy().transpose(1, 0, 2)], axis=1).astype(np.float64)
+    for t in range(steps):
+        L = T + t + 1
+        attended = c.is_hi[:, :L].copy()
+        attended[:, L - 1] = True               # the appended token is attended
+        o, p = c.step(q[t, 0][:, None].numpy(), kn[t, 0].numpy(), vn[t, 0].numpy(), SCALE, kh, W)
+        for h in range(H):
+            keep = attended[h]
+            tq = torch.from_numpy(q[t, 0, h].numpy().astype(np.float64))[None, None, None, :]
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                tq, torch.from_numpy(K_all[h, :L][keep])[None, None], torch.from_numpy(V_all[h, :L][keep])[None, None],
+                scale=SCALE)[0, 0, 0].numpy()
+            np.testing.assert_allclose(o[h, 0], ref, rtol=1e-6, atol=1e-6)
+            assert (p[h, 0, ~keep] == 0).all()
+            assert abs(float(p[h, 0, keep].sum(dtype=np.float64)) - 1.0) < 1e-5
+        assert (c.is_hi[:, :L].sum(1) == kh + W).all()
+        assert not (c.is_hi[:, :L] & ~attended).any()
+
+
 def test_step_invariants_and_demotion_path():
     wl = workloads.WORKLOADS["tiny"]
     wl, k, v, sc, q, kn, vn = _tiny_inputs(wl, 200, 6, seed=3)
