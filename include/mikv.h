@@ -139,6 +139,33 @@ int mikv_balance_channels(const uint16_t *q_prefill, const uint16_t *k_prefill, 
                           float *balance, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Importance scores of the prompt (the H2O accumulated attention at the end
+ * of prefill that ranks tokens for the first selection, Section 3.1 and the
+ * H2O policy of Section 4.1): with causal softmax attention over the prompt,
+ *   scores[b, h, j] = sum_{g in group(h)} sum_{i = j}^{T-1} softmax_i(scale * q[b, g, i] . k[b, h, :])_j
+ * where group(h) are the Hq / Hkv query heads sharing KV head h.  Logits are
+ * fp16 x fp16 products accumulated in fp32 on the matrix cores; the sums
+ * are fp32 (summation order: per query head, query rows in ascending order,
+ * then the heads of the group), so results are reproducible run to run but
+ * not bit-identical to another summation order.
+ *   q_prefill fp16 [B, Hq, T, 128]; k_prefill fp16 [B, Hkv, T, 128], both
+ *             16-byte aligned (the prompt's keys as computed, before any
+ *             balancing or quantization: balancing leaves q . k unchanged);
+ *   scale     softmax scale (1/sqrt(128) for the paper's models), > 0;
+ *   scores    fp32 [B, Hkv, T] (output), the `scores` argument of
+ *             mikv_select_prefill and the score_init of mikv_quantize_kv;
+ *   workspace device bytes, at least mikv_prefill_importance_workspace_size(B, Hq, T)
+ *             (per-query softmax statistics).
+ * Errors: INVALID_ARG for null or misaligned pointers, T < 1, Hq % Hkv != 0,
+ * scale <= 0; UNSUPPORTED for head_dim != 128 or Hq / Hkv not in {1,2,4,8};
+ * CAPACITY for a too-small workspace.
+ */
+size_t mikv_prefill_importance_workspace_size(int32_t batch, int32_t q_heads, int32_t tokens);
+int mikv_prefill_importance(const uint16_t *q_prefill, const uint16_t *k_prefill, int32_t batch,
+                            int32_t q_heads, int32_t kv_heads, int32_t tokens, int32_t head_dim, float scale,
+                            float *scores, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * Raw per-token grouped asymmetric quantizer, Section 3.1, Eq. 1, on rows of
  * 128 channels (for unit use and testing):
  *   x_c   = fp32(x[r, c]) * balance[r / rows_per_balance, c]   (balance nullable: x_c = fp32(x))

@@ -66,3 +66,26 @@ def select(acc, is_hi, length: int, k_heavy: int, window: int, initial: bool) ->
     new_hi = in_window.copy()
     new_hi[keep] = True
     return new_hi
+
+
+def prefill_importance(q16, k16, scale: float) -> np.ndarray:
+    """H2O importance of the prompt tokens at the end of prefill.
+
+    q16 fp16 [G, T, D] (the query heads sharing one KV head); k16 fp16 [T, D].
+    Every prompt query i attends causally to keys 0..i; token j's score is
+    the sum, over the G query heads and every query i >= j, of its softmax
+    probability.  Computed in fp64 from the fp16 inputs; returned as fp32 [T].
+    """
+    q = np.asarray(q16, dtype=np.float16).astype(np.float64)
+    k = np.asarray(k16, dtype=np.float16).astype(np.float64)
+    G, T, _ = q.shape
+    causal = np.tril(np.ones((T, T), dtype=bool))          # [query i, key j]: j <= i
+    total = np.zeros(T, dtype=np.float64)
+    for g in range(G):
+        s = (q[g] @ k.T) * float(scale)
+        s = np.where(causal, s, -np.inf)
+        s = s - s.max(axis=1, keepdims=True)
+        e = np.where(causal, np.exp(s), 0.0)
+        p = e / e.sum(axis=1, keepdims=True)
+        total += p.sum(axis=0)
+    return total.astype(np.float32)

@@ -49,6 +49,9 @@ _SIGS = {
     "mikv_balance_workspace_size": (c_size_t, [c_int32, c_int32, c_int32]),
     "mikv_balance_channels": (c_int32, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_int32,
                                         c_void_p, c_void_p, c_size_t, c_void_p]),
+    "mikv_prefill_importance_workspace_size": (c_size_t, [c_int32, c_int32, c_int32]),
+    "mikv_prefill_importance": (c_int32, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_int32, c_float,
+                                          c_void_p, c_void_p, c_size_t, c_void_p]),
     "mikv_quantize_rows": (c_int32, [c_void_p, c_int64, c_int32, c_void_p, c_int32, c_int32, c_int32,
                                      c_void_p, c_void_p, c_void_p]),
     "mikv_quantize_workspace_size": (c_size_t, [_PC, c_int32]),
@@ -192,6 +195,24 @@ def mikv_balance_channels(q_prefill: torch.Tensor, k_prefill: torch.Tensor, bala
     ws = workspace if workspace is not None else _workspace(nbytes, q_prefill.device)
     _check(L.mikv_balance_channels(_ptr(q_prefill), _ptr(k_prefill), B, Hq, Hkv, T, D, _ptr(balance), _ptr(ws),
                                    ws.numel(), _stream()), "mikv_balance_channels")
+
+
+def mikv_prefill_importance(q_prefill: torch.Tensor, k_prefill: torch.Tensor, scores: torch.Tensor,
+                            scale: Optional[float] = None, workspace: Optional[torch.Tensor] = None):
+    """H2O importance of the prompt tokens: column sums of causal softmax
+    attention over the prompt, summed over each KV head's query heads.
+    q_prefill fp16 [B, Hq, T, 128], k_prefill fp16 [B, Hkv, T, 128] -> scores fp32 [B, Hkv, T]."""
+    B, Hq, T, D = q_prefill.shape
+    Hkv = k_prefill.shape[1]
+    _require(q_prefill, torch.float16, name="q_prefill")
+    _require(k_prefill, torch.float16, (B, Hkv, T, D), "k_prefill")
+    _require(scores, torch.float32, (B, Hkv, T), "scores")
+    L = lib()
+    nbytes = L.mikv_prefill_importance_workspace_size(B, Hq, T)
+    ws = workspace if workspace is not None else _workspace(nbytes, q_prefill.device)
+    scale = 1.0 / math.sqrt(D) if scale is None else scale
+    _check(L.mikv_prefill_importance(_ptr(q_prefill), _ptr(k_prefill), B, Hq, Hkv, T, D, scale, _ptr(scores),
+                                     _ptr(ws), ws.numel(), _stream()), "mikv_prefill_importance")
 
 
 def mikv_quantize_rows(x: torch.Tensor, bits: int, group: int, codes: torch.Tensor, params: torch.Tensor,

@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 16
+    assert len(names) == 18
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -91,6 +91,15 @@ def test_null_pointers_and_capacity():
     # 16-byte alignment of the prefill rows (checked on the host, nothing launched)
     assert L.mikv_balance_channels(ctypes.c_void_p(0x1002), ctypes.c_void_p(0x1000), 1, 4, 4, 8, 128,
                                    ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), 1 << 20, None) == 1
+    # prefill importance: host-side validation, nothing launched
+    assert L.mikv_prefill_importance(None, None, 1, 2, 2, 8, 128, ctypes.c_float(0.1), None, None, 0, None) == 1
+    assert L.mikv_prefill_importance(qk_ := ctypes.c_void_p(0x1000), qk_, 1, 2, 2, 8, 64, ctypes.c_float(0.1),
+                                     qk_, qk_, 1 << 20, None) == 2
+    assert L.mikv_prefill_importance(qk_, qk_, 1, 6, 2, 8, 128, ctypes.c_float(0.1), qk_, qk_, 1 << 20, None) == 2
+    assert L.mikv_prefill_importance(ctypes.c_void_p(0x1008), qk_, 1, 2, 2, 8, 128, ctypes.c_float(0.1), qk_, qk_,
+                                     1 << 20, None) == 1
+    assert L.mikv_prefill_importance(qk_, qk_, 1, 2, 2, 8, 128, ctypes.c_float(0.1), qk_, qk_, 8, None) == 3
+    assert L.mikv_prefill_importance_workspace_size(1, 2, 8) == 2 * 8 * 8
     assert L.mikv_importance_update(ctypes.byref(_desc()), 4, None, None) == 1
     qk = ctypes.c_void_p(0x1000)
     assert L.mikv_quantize_kv(ctypes.byref(_desc()), qk, qk, None, 10, 8, None, None, None, 0, None) == 3

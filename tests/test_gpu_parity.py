@@ -12,7 +12,7 @@ import torch
 
 import oracle
 from paper_2402_18096_amd import mikv, workloads
-from tests.parity import Lockstep, SampledLockstep, compare_state, np16
+from tests.parity import SCALE, Lockstep, SampledLockstep, compare_state, np16
 from tests.quant_inputs import tie_rows
 
 pytestmark = pytest.mark.gpu
@@ -235,6 +235,44 @@ def test_full_size_eviction_sampled_heads():
         run.step(t)
     del run
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,shape", [
+    ("tiny", dict(batch=1, q_heads=2, kv_heads=2, context=300)),          # ragged: not a multiple of 64
+    ("mistral_7b", dict(batch=2, q_heads=8, kv_heads=2, context=200)),    # GQA 4, outliers x20
+    ("llama2_13b", dict(batch=1, q_heads=2, kv_heads=2, context=1000)),   # Student-t keys
+    ("long_context", dict(batch=1, q_heads=2, kv_heads=1, context=17)),   # GQA 2, one partial tile
+    ("tiny", dict(batch=1, q_heads=1, kv_heads=1, context=1)),            # a single token
+])
+def test_prefill_importance_matches_oracle(name, shape):
+    """H2O importance of the prompt (column sums of causal softmax attention,
+    summed over the query heads of each KV head) against the fp64 oracle;
+    fp32 sums in another order, so within 1e-4 relative, and the total mass
+    G * T of every head.  The prefill selection over these scores then
+    matches the oracle's selection over the same scores bit for bit."""
+    dev = _dev()
+    wl = workloads.small_workload(name, **shape)
+    k, _ = workloads.prefill_kv(wl, dev)
+    q = workloads.prefill_queries(wl, dev)
+    got = torch.empty(wl.batch, wl.kv_heads, wl.context, dtype=torch.float32, device=dev)
+    mikv.mikv_prefill_importance(q, k, got, SCALE)
+    torch.cuda.synchronize()
+    got = got.cpu().numpy().reshape(wl.n_heads, wl.context)
+    G, T = wl.group_size, wl.context
+    qn = np16(q).reshape(wl.n_heads, G, T, 128)
+    kn = np16(k).reshape(wl.n_heads, T, 128)
+    for h in range(wl.n_heads):
+        ref = oracle.prefill_importance(qn[h], kn[h], SCALE)
+        np.testing.assert_allclose(got[h], ref, rtol=1e-4, atol=1e-6, err_msg=f"{name} head {h}")
+        assert abs(float(got[h].sum(dtype=np.float64)) - G * T) < 1e-4 * G * T
+    if T > 40:
+        kh, W = T // 5, 16
+        mask = torch.empty(wl.batch, wl.kv_heads, T, dtype=torch.uint8, device=dev)
+        mikv.mikv_select_prefill(torch.from_numpy(got).reshape(wl.batch, wl.kv_heads, T).to(dev), kh, W, mask)
+        torch.cuda.synchronize()
+        m = mask.cpu().numpy().reshape(wl.n_heads, T).astype(bool)
+        for h in range(wl.n_heads):
+            np.testing.assert_array_equal(m[h], oracle.select(got[h], None, T, kh, W, initial=True))
 
 
 def test_capacity_overflow_sets_status_without_writing_out_of_bounds():

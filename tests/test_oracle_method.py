@@ -178,6 +178,61 @@ def test_select_invariants():
     assert new.sum() == W + min(k, int(is_hi[:-W].sum()))
 
 
+# -- prefill importance (H2O accumulated attention over the prompt) ----------
+
+def _prefill_importance_brute_force(q, k, scale):
+    """Pure-Python loops: for every query row, a causal softmax, added into
+    the scores of the keys it attends to."""
+    G, T, D = len(q), len(k), len(k[0])
+    out = [0.0] * T
+    for g in range(G):
+        for i in range(T):
+            s = [sum(float(q[g][i][c]) * float(k[j][c]) for c in range(D)) * scale for j in range(i + 1)]
+            m = max(s)
+            e = [math.exp(x - m) for x in s]
+            z = sum(e)
+            for j in range(i + 1):
+                out[j] += e[j] / z
+    return out
+
+
+def test_prefill_importance_brute_force_small():
+    rng = np.random.default_rng(11)
+    q = rng.standard_normal((2, 7, 5)).astype(np.float16)
+    k = rng.standard_normal((7, 5)).astype(np.float16)
+    got = oracle.prefill_importance(q, k, 0.7)
+    np.testing.assert_allclose(got, _prefill_importance_brute_force(q, k, 0.7), rtol=1e-6, atol=1e-7)
+
+
+def test_prefill_importance_equal_keys_harmonic_tail():
+    """All keys equal: query i spreads 1/(i+1) over keys 0..i, so key j
+    collects G * (H_T - H_j), H the harmonic numbers."""
+    T, G = 40, 3
+    q = np.random.default_rng(2).standard_normal((G, T, 8)).astype(np.float16)
+    k = np.tile(np.random.default_rng(3).standard_normal((1, 8)).astype(np.float16), (T, 1))
+    H = np.concatenate([[0.0], np.cumsum(1.0 / np.arange(1, T + 1))])
+    np.testing.assert_allclose(oracle.prefill_importance(q, k, 0.3), G * (H[T] - H[:T]), rtol=1e-6)
+
+
+def test_prefill_importance_mass_and_first_token():
+    """Each query's probabilities sum to 1 (total mass G*T); the last key is
+    attended by the last query only, the first key by every query."""
+    T, G = 33, 2
+    rng = np.random.default_rng(4)
+    q = rng.standard_normal((G, T, 16)).astype(np.float16)
+    k = rng.standard_normal((T, 16)).astype(np.float16)
+    sc = oracle.prefill_importance(q, k, 0.25)
+    assert abs(float(sc.sum(dtype=np.float64)) - G * T) < 1e-3
+    qq, kk = q.astype(np.float64), k.astype(np.float64)
+    last = 0.0
+    for g in range(G):
+        s = qq[g, T - 1] @ kk.T * 0.25
+        e = np.exp(s - s.max())
+        last += e[T - 1] / e.sum()
+    np.testing.assert_allclose(sc[T - 1], last, rtol=1e-6)
+    assert sc[0] >= 1.0 * G - 1e-6            # query 0 gives key 0 probability 1
+
+
 def test_heavy_budget():
     assert oracle.heavy_budget(513, 1, 5, 32, False) == 102
     assert oracle.heavy_budget(4097, 1, 4, 64, True) == 960
