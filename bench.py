@@ -154,6 +154,49 @@ def copy_probe(mb: int):
     print(json.dumps(rec), flush=True)
 
 
+MFMA_FP16_PEAK_TFLOPS = 2500.0  # dense fp16 matrix-core peak of one MI355X
+
+
+def prefill_importance_probe(workload: str, reps: int):
+    """Time mikv_prefill_importance on the workload's prompt (its seeded fp16
+    queries and keys): the H2O importance of every prompt token.  Algorithmic
+    FLOPs are those of one causal Q K^T (2 * 128 per query-key pair with
+    key <= query, every query head); the kernel computes the logits twice
+    (statistics pass, then column-sum pass)."""
+    import torch
+
+    from paper_2402_18096_amd import mikv, workloads
+    wl = workloads.WORKLOADS[workload]
+    dev = torch.device("cuda:0")
+    k, v = workloads.prefill_kv(wl, dev)
+    del v
+    q = workloads.prefill_queries(wl, dev)
+    scores = torch.empty(wl.batch, wl.kv_heads, wl.context, dtype=torch.float32, device=dev)
+    ws = torch.empty(mikv.lib().mikv_prefill_importance_workspace_size(wl.batch, wl.q_heads, wl.context),
+                     dtype=torch.uint8, device=dev)
+    scale = 1.0 / math.sqrt(wl.head_dim)
+    mikv.mikv_prefill_importance(q, k, scores, scale, ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        mikv.mikv_prefill_importance(q, k, scores, scale, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    T = wl.context
+    flops = 2.0 * wl.head_dim * (T * (T + 1) / 2) * wl.batch * wl.q_heads
+    tflops = flops / (ms * 1e-3) / 1e12
+    mass = float(scores.double().sum()) / (wl.batch * wl.q_heads * T)
+    rec = {"prefill_importance": {"workload": wl.name, "batch": wl.batch, "q_heads": wl.q_heads,
+                                  "kv_heads": wl.kv_heads, "tokens": T, "ms": round(ms, 3),
+                                  "algorithmic_tflop": round(flops / 1e12, 3), "achieved_tflops": round(tflops, 1),
+                                  "peak_tflops": MFMA_FP16_PEAK_TFLOPS, "frac": round(tflops / MFMA_FP16_PEAK_TFLOPS, 4),
+                                  "mass_per_query": round(mass, 6), "reps": reps,
+                                  "note": "the kernel evaluates the logits twice (statistics, then column sums)"}}
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -177,6 +220,8 @@ def main():
                     help="untimed steps after the phase pass, each bracketed by two events: this many with the "
                          "caches as the previous step left them (warm), then this many each preceded by a "
                          "1 GiB read that evicts the 256 MB last-level cache (cold)")
+    ap.add_argument("--prefill-importance", action="store_true",
+                    help="instead of the bench: time the prompt-importance kernel on the workload's prompt")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
                     help="instead of the bench: time a plain device-to-device copy of MB megabytes")
     args = ap.parse_args()
@@ -192,6 +237,8 @@ def main():
 
     if args.copy_probe:
         return copy_probe(args.copy_probe)
+    if args.prefill_importance:
+        return prefill_importance_probe(args.workload, max(1, args.steps if args.steps < 256 else 3))
     wl = workloads.WORKLOADS[args.workload]
     for ov in args.override:
         key, val = ov.split("=", 1)

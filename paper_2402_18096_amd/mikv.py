@@ -371,11 +371,18 @@ class MikvDecoder:
         wl = self.wl
         return heavy_budget(length, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio)
 
-    def prefill(self, k: torch.Tensor, v: torch.Tensor, scores: torch.Tensor,
+    def prefill(self, k: torch.Tensor, v: torch.Tensor, scores: Optional[torch.Tensor],
                 q_prefill: Optional[torch.Tensor] = None):
-        """k, v fp16 [B, Hkv, T, D]; scores fp32 [B, Hkv, T]; q_prefill fp16
-        [B, Hq, T, D] when the workload balances keys and queries."""
+        """k, v fp16 [B, Hkv, T, D]; scores fp32 [B, Hkv, T], or None to use the
+        prompt's own H2O importance (mikv_prefill_importance, which needs
+        q_prefill); q_prefill fp16 [B, Hq, T, D] (also when the workload
+        balances keys and queries)."""
         wl, T = self.wl, k.shape[2]
+        if scores is None:
+            if q_prefill is None:
+                raise MikvError("prefill: the prompt's importance needs q_prefill")
+            scores = torch.empty(wl.batch, wl.kv_heads, T, dtype=torch.float32, device=self.device)
+            mikv_prefill_importance(q_prefill, k, scores)
         if wl.balanced:
             self.balance = torch.empty(wl.batch, wl.kv_heads, HEAD_DIM, dtype=torch.float32, device=self.device)
             mikv_balance_channels(q_prefill, k, self.balance)

@@ -275,6 +275,26 @@ def test_prefill_importance_matches_oracle(name, shape):
             np.testing.assert_array_equal(m[h], oracle.select(got[h], None, T, kh, W, initial=True))
 
 
+def test_lockstep_with_prompt_importance():
+    """A decode run whose first selection uses the prompt's own H2O scores
+    (mikv_prefill_importance) instead of seeded ones: the oracle takes the
+    GPU's scores (the lockstep protocol) and every later step stays exact."""
+    _dev()
+    wl = workloads.small_workload("long_context", batch=1, q_heads=2, kv_heads=2, context=1500)
+    run = Lockstep(wl, 3)
+    q = workloads.prefill_queries(wl, "cuda")
+    sc = torch.empty(wl.batch, wl.kv_heads, wl.context, dtype=torch.float32, device="cuda")
+    mikv.mikv_prefill_importance(q, run.k.cuda(), sc, SCALE)
+    torch.cuda.synchronize()
+    ref = oracle.prefill_importance(np16(q).reshape(2, 1, wl.context, 128)[0], np16(run.k).reshape(2, wl.context, 128)[0],
+                                    SCALE)
+    np.testing.assert_allclose(sc.cpu().numpy().reshape(2, -1)[0], ref, rtol=1e-4, atol=1e-6)
+    run.sc = sc.cpu()
+    run.prefill()
+    for t in range(3):
+        run.step(t)
+
+
 def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
     dev = _dev()
     c = mikv.MikvCache(1, 2, 2, 32, 16, 2, cap_hi=4, cap_lo=32, max_len=64, device=dev)
