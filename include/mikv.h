@@ -71,6 +71,9 @@ enum mikv_attention_flags {
  *   hi_bits == 16: hi_k, hi_v are fp16 [NH, cap_hi, 128]; hi_kp, hi_vp unused.
  *   hi_bits == 8 : hi_k, hi_v are uint8 codes [NH, cap_hi, 128];
  *                  hi_kp, hi_vp are fp16 (alpha, beta) pairs [NH, cap_hi, 128/group, 2].
+ *   hi_bits == 4 : the INT4 importance cache of Table 3 (with lo_bits 2 or 0):
+ *                  hi_k, hi_v are packed codes [NH, cap_hi, 64] (LSB first, as
+ *                  the retained pool's); hi_kp, hi_vp as for INT8.
  *   hi_pos  [NH, cap_hi] int32: token position held by each slot.
  *   hi_acc  [NH, cap_hi] fp32 : the token's accumulated attention (H2O score).
  *   n_hi    [NH] int32        : occupied slots (slots [0, n_hi) are valid).
@@ -100,7 +103,7 @@ typedef struct mikv_cache {
   int32_t kv_heads;   /* q_heads % kv_heads == 0; q_heads / kv_heads in {1,2,4,8} */
   int32_t head_dim;   /* 128 */
   int32_t group;      /* quantization group size: 32, 64 or 128 channels */
-  int32_t hi_bits;    /* 16 (fp16) or 8 (INT8) */
+  int32_t hi_bits;    /* 16 (fp16), 8 (INT8) or 4 (INT4, with lo_bits 2 or 0) */
   int32_t lo_bits;    /* 2, 4 or 8; 0 = evict instead of retaining (see above) */
   int32_t cap_hi;     /* importance-pool slots per head */
   int32_t cap_lo;     /* retained-pool slots per head (ignored when lo_bits is 0) */

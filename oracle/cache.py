@@ -40,7 +40,7 @@ class OracleCache:
 
     def __init__(self, n_heads: int, group_size: int, max_len: int, hi_bits: int, lo_bits: int,
                  group: int, head_dim: int = 128):
-        assert hi_bits in (16, 8) and lo_bits in (0, 2, 4, 8)
+        assert hi_bits in (16, 8, 4) and lo_bits in (0, 2, 4, 8)
         self.n_heads, self.G, self.max_len = n_heads, group_size, max_len
         self.hi_bits, self.lo_bits, self.group, self.d = hi_bits, lo_bits, group, head_dim
         ng = head_dim // group
@@ -65,8 +65,9 @@ class OracleCache:
             self.hk[h, pos] = f16_bits(kx)
             self.hv[h, pos] = f16_bits(vx)
         else:
-            self.hk[h, pos], self.hk_a[h, pos], self.hk_b[h, pos] = quantize(kx, 8, self.group)
-            self.hv[h, pos], self.hv_a[h, pos], self.hv_b[h, pos] = quantize(vx, 8, self.group)
+            n = self.hi_bits  # INT8, or INT4 (Table 3's INT4 importance cache)
+            self.hk[h, pos], self.hk_a[h, pos], self.hk_b[h, pos] = quantize(kx, n, self.group)
+            self.hv[h, pos], self.hv_a[h, pos], self.hv_b[h, pos] = quantize(vx, n, self.group)
 
     def _store_lo(self, h, pos, kx, vx):
         n = self.lo_bits

@@ -39,8 +39,10 @@ int validate_cache(const mikv_cache *c) {
     return set_error(MIKV_ERR_UNSUPPORTED, "head_dim must be 128 (got %d)", c->head_dim);
   if (c->group != 32 && c->group != 64 && c->group != 128)
     return set_error(MIKV_ERR_UNSUPPORTED, "group must be 32, 64 or 128 (got %d)", c->group);
-  if (c->hi_bits != 16 && c->hi_bits != 8)
-    return set_error(MIKV_ERR_UNSUPPORTED, "hi_bits must be 16 or 8 (got %d)", c->hi_bits);
+  if (c->hi_bits != 16 && c->hi_bits != 8 && c->hi_bits != 4)
+    return set_error(MIKV_ERR_UNSUPPORTED, "hi_bits must be 16, 8 or 4 (got %d)", c->hi_bits);
+  if (c->hi_bits == 4 && c->lo_bits != 2 && c->lo_bits != 0)
+    return set_error(MIKV_ERR_UNSUPPORTED, "an INT4 importance pool needs lo_bits 2 or 0 (got %d)", c->lo_bits);
   if (c->lo_bits != 0 && c->lo_bits != 2 && c->lo_bits != 4 && c->lo_bits != 8)
     return set_error(MIKV_ERR_UNSUPPORTED, "lo_bits must be 0, 2, 4 or 8 (got %d)", c->lo_bits);
   if (c->cap_hi < 1 || (!evicting(c) && c->cap_lo < 1) || c->max_len < 1)
@@ -52,8 +54,8 @@ int validate_cache(const mikv_cache *c) {
   if (!c->hi_k || !c->hi_v || !c->hi_pos || !c->hi_acc || !c->n_hi || !c->n_lo || !c->status ||
       (!evicting(c) && (!c->lo_k || !c->lo_v || !c->lo_kp || !c->lo_vp || !c->lo_pos)))
     return set_error(MIKV_ERR_INVALID_ARG, "a required cache pointer is NULL");
-  if (c->hi_bits == 8 && (!c->hi_kp || !c->hi_vp))
-    return set_error(MIKV_ERR_INVALID_ARG, "hi_kp/hi_vp are required for an INT8 importance pool");
+  if (c->hi_bits != 16 && (!c->hi_kp || !c->hi_vp))
+    return set_error(MIKV_ERR_INVALID_ARG, "hi_kp/hi_vp are required for an INT8 or INT4 importance pool");
   return MIKV_OK;
 }
 

@@ -103,9 +103,9 @@ __device__ inline void append_row(const AppendArgs &P, int h, int slot, int lane
     for (int i = 0; i < 4; ++i) d4[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
   } else {
     const int ng = kHeadDim / P.group;
-    uint8_t *dst = lane_pick(is_v, P.hi_v, P.hi_k) + row * kHeadDim + lane4 * 32;
+    uint8_t *dst = lane_pick(is_v, P.hi_v, P.hi_k) + row * (kHeadDim * HI_BITS / 8) + lane4 * (32 * HI_BITS / 8);
     uint32_t *par = lane_pick(is_v, P.hi_vp, P.hi_kp) + row * ng + (lane4 * 32) / P.group;
-    quantize_segment<8>(x, P.group, lane4, dst, par, true);
+    quantize_segment<HI_BITS>(x, P.group, lane4, dst, par, true);
   }
   if (lane8 == 0) {
     P.hi_pos[row] = P.pos;

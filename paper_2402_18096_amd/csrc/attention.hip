@@ -1543,6 +1543,7 @@ int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const
     case 1604: launch_partial_g<16, 4>(A, G, grid, st); break;
     case 1608: launch_partial_g<16, 8>(A, G, grid, st); break;
     case 802: launch_partial_g<8, 2>(A, G, grid, st); break;
+    case 402: launch_partial_g<4, 2>(A, G, grid, st); break;
     case 804: launch_partial_g<8, 4>(A, G, grid, st); break;
     default: launch_partial_g<8, 8>(A, G, grid, st); break;
   }
@@ -1580,6 +1581,7 @@ int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *
     case 1604: launch_finalize_select<16, 4>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 1608: launch_finalize_select<16, 8>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 802: launch_finalize_select<8, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    case 402: launch_finalize_select<4, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 804: launch_finalize_select<8, 4>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     default: launch_finalize_select<8, 8>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
   }

@@ -229,9 +229,10 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
           for (int i = 0; i < 4; ++i) d4[i] = make_uint4(w[4 * i], w[4 * i + 1], w[4 * i + 2], w[4 * i + 3]);
         }
       } else {
-        uint8_t *dst = (is_v ? P.hi_v : P.hi_k) + ((int64_t)h * P.cap_hi + sl) * kHeadDim + lane4 * 32;
+        uint8_t *dst = (is_v ? P.hi_v : P.hi_k) + ((int64_t)h * P.cap_hi + sl) * (kHeadDim * HI_BITS / 8) +
+                       lane4 * (32 * HI_BITS / 8);
         uint32_t *par = (is_v ? P.hi_vp : P.hi_kp) + ((int64_t)h * P.cap_hi + sl) * ng + (lane4 * 32) / P.group;
-        quantize_segment<8>(x, P.group, lane4, dst, par, store);
+        quantize_segment<HI_BITS>(x, P.group, lane4, dst, par, store);
       }
     } else if (P.evict) {
       // evicted token (no retained pool): nothing to store; the four lanes
@@ -386,6 +387,7 @@ extern "C" int mikv_quantize_kv(const mikv_cache *c, const uint16_t *k, const ui
     case 1604: launch_place<16, 4>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 1608: launch_place<16, 8>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 802: launch_place<8, 2>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
+    case 402: launch_place<4, 2>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 804: launch_place<8, 4>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     default: launch_place<8, 8>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
   }

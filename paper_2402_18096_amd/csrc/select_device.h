@@ -155,7 +155,7 @@ __device__ inline void load_hi_segment(const SelArgs &A, const uint8_t *rows, co
         x[i * 8 + 2 * j + 1] = f16_to_f32((uint16_t)(ws[j] >> 16));
       }
     }
-  } else {
+  } else if constexpr (HI_BITS == 8) {
     const uint4 *s4 = reinterpret_cast<const uint4 *>(rows + slot * kHeadDim + part * 32);
     const uint32_t par = pars[slot * (kHeadDim / A.group) + (part * 32) / A.group];
     const float a = f16_to_f32((uint16_t)(par & 0xffffu)), b = f16_to_f32((uint16_t)(par >> 16));
@@ -166,6 +166,13 @@ __device__ inline void load_hi_segment(const SelArgs &A, const uint8_t *rows, co
 #pragma unroll
       for (int j = 0; j < 16; ++j) x[i * 16 + j] = fmaf(a, (float)((ws[j >> 2] >> (8 * (j & 3))) & 0xffu), b);
     }
+  } else {  // INT4: 32 codes in 16 bytes, channel c at bits 4c
+    const uint4 w = *reinterpret_cast<const uint4 *>(rows + slot * (kHeadDim / 2) + part * 16);
+    const uint32_t par = pars[slot * (kHeadDim / A.group) + (part * 32) / A.group];
+    const float a = f16_to_f32((uint16_t)(par & 0xffffu)), b = f16_to_f32((uint16_t)(par >> 16));
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int j = 0; j < 32; ++j) x[j] = fmaf(a, (float)((ws[j >> 3] >> (4 * (j & 7))) & 0xfu), b);
   }
 }
 
@@ -215,7 +222,7 @@ template <int HI_BITS, int LO_BITS>
 __device__ inline void demote_row(const SelArgs &A, int h, int slot, int64_t lslot, int p) {
   if (threadIdx.x >= 8) return;
   const int ng = kHeadDim / A.group;
-  const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim * HI_BITS / 8;
   const int is_v = threadIdx.x >> 2, part = threadIdx.x & 3;
   const uint8_t *rows = lane_pick(is_v, A.hi_v, A.hi_k) + (int64_t)h * A.cap_hi * hrow;
   const uint32_t *pars = HI_BITS == 16 ? nullptr : lane_pick(is_v, A.hi_vp, A.hi_kp) + (int64_t)h * A.cap_hi * ng;
@@ -242,7 +249,7 @@ struct SlotData {
 
 template <int HI_BITS>
 __device__ inline SlotData<HI_BITS> load_slot(const SelArgs &A, int h, int src) {
-  constexpr int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  constexpr int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim * HI_BITS / 8;
   constexpr int chunks = hrow / 16;
   const int ng = kHeadDim / A.group;
   SlotData<HI_BITS> d{};
@@ -250,7 +257,7 @@ __device__ inline SlotData<HI_BITS> load_slot(const SelArgs &A, int h, int src) 
     const uint8_t *base = lane_pick(threadIdx.x < chunks, A.hi_k, A.hi_v) + (int64_t)h * A.cap_hi * hrow;
     d.piece = reinterpret_cast<const uint4 *>(base + (int64_t)src * hrow)[threadIdx.x % chunks];
   }
-  if (HI_BITS == 8 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
+  if (HI_BITS != 16 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
     const uint32_t *pp = lane_pick(threadIdx.x - 64 < (unsigned)ng, A.hi_kp, A.hi_vp);
     d.par = pp[((int64_t)h * A.cap_hi + src) * ng + (threadIdx.x - 64) % ng];
   }
@@ -263,14 +270,14 @@ __device__ inline SlotData<HI_BITS> load_slot(const SelArgs &A, int h, int src) 
 
 template <int HI_BITS>
 __device__ inline void store_slot(const SelArgs &A, int h, int dst, const SlotData<HI_BITS> &d) {
-  constexpr int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  constexpr int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim * HI_BITS / 8;
   constexpr int chunks = hrow / 16;
   const int ng = kHeadDim / A.group;
   if (threadIdx.x < 2 * chunks) {
     uint8_t *base = lane_pick(threadIdx.x < chunks, A.hi_k, A.hi_v) + (int64_t)h * A.cap_hi * hrow;
     reinterpret_cast<uint4 *>(base + (int64_t)dst * hrow)[threadIdx.x % chunks] = d.piece;
   }
-  if (HI_BITS == 8 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
+  if (HI_BITS != 16 && threadIdx.x >= 64 && threadIdx.x < 64 + 2 * ng) {
     uint32_t *pp = lane_pick(threadIdx.x - 64 < (unsigned)ng, A.hi_kp, A.hi_vp);
     pp[((int64_t)h * A.cap_hi + dst) * ng + (threadIdx.x - 64) % ng] = d.par;
   }
@@ -381,7 +388,7 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
 
   // re-quantize the demoted tokens into the retained pool (4 lanes per row)
   const int ng = kHeadDim / A.group;
-  const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim;
+  const int64_t hrow = HI_BITS == 16 ? 2 * kHeadDim : kHeadDim * HI_BITS / 8;
   for (int r = threadIdx.x >> 2; r < (A.evict ? 0 : 2 * n_dem); r += kSel / 4) {
     const int d = r >> 1, is_v = r & 1, part = threadIdx.x & 3;
     const int slot = dem_list[d];
@@ -418,7 +425,7 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
     const int src = fill_list[f], dst = dem_list[f];
     A.hi_pos[(int64_t)h * A.cap_hi + dst] = pos[src];
     A.hi_acc[(int64_t)h * A.cap_hi + dst] = acc[src];
-    if (HI_BITS == 8) {
+    if (HI_BITS != 16) {
       for (int g = 0; g < ng; ++g) {
         A.hi_kp[((int64_t)h * A.cap_hi + dst) * ng + g] = A.hi_kp[((int64_t)h * A.cap_hi + src) * ng + g];
         A.hi_vp[((int64_t)h * A.cap_hi + dst) * ng + g] = A.hi_vp[((int64_t)h * A.cap_hi + src) * ng + g];

@@ -146,7 +146,8 @@ class MikvCache:
             self.hi_k, self.hi_v = z(NH, cap_hi, D, dt=torch.float16), z(NH, cap_hi, D, dt=torch.float16)
             self.hi_kp = self.hi_vp = None
         else:
-            self.hi_k, self.hi_v = z(NH, cap_hi, D, dt=torch.uint8), z(NH, cap_hi, D, dt=torch.uint8)
+            hrow = D * hi_bits // 8  # INT8 or INT4 codes, packed
+            self.hi_k, self.hi_v = z(NH, cap_hi, hrow, dt=torch.uint8), z(NH, cap_hi, hrow, dt=torch.uint8)
             self.hi_kp, self.hi_vp = z(NH, cap_hi, ng, 2, dt=torch.int16), z(NH, cap_hi, ng, 2, dt=torch.int16)
         self.hi_pos = z(NH, cap_hi, dt=torch.int32)
         self.hi_acc = z(NH, cap_hi, dt=torch.float32)

@@ -90,9 +90,10 @@ def compare_state(c: mikv.MikvCache, orc: oracle.OracleCache, heads=None, tag=""
         if s["map"] is not None:
             np.testing.assert_array_equal(s["map"][gh, :L].astype(bool), pos_hi, err_msg=f"{tag} head {gh}: map")
         # importance pool contents and scores
-        np.testing.assert_array_equal(s["hk"][gh, :nh], orc.hk[oh, hp], err_msg=f"{tag} head {gh}: hi K")
-        np.testing.assert_array_equal(s["hv"][gh, :nh], orc.hv[oh, hp], err_msg=f"{tag} head {gh}: hi V")
-        if orc.hi_bits == 8:
+        hpk = (lambda x: x) if orc.hi_bits in (16, 8) else (lambda x: oracle.pack(x, orc.hi_bits))
+        np.testing.assert_array_equal(s["hk"][gh, :nh], hpk(orc.hk[oh, hp]), err_msg=f"{tag} head {gh}: hi K")
+        np.testing.assert_array_equal(s["hv"][gh, :nh], hpk(orc.hv[oh, hp]), err_msg=f"{tag} head {gh}: hi V")
+        if orc.hi_bits != 16:
             np.testing.assert_array_equal(s["hkp"][gh, :nh, :, 0], orc.hk_a[oh, hp], err_msg=f"{tag} hi K alpha")
             np.testing.assert_array_equal(s["hkp"][gh, :nh, :, 1], orc.hk_b[oh, hp], err_msg=f"{tag} hi K beta")
             np.testing.assert_array_equal(s["hvp"][gh, :nh, :, 0], orc.hv_a[oh, hp], err_msg=f"{tag} hi V alpha")

@@ -49,13 +49,18 @@ def _call_attention(c, length=4, ws_bytes=1 << 30):
 
 
 @pytest.mark.parametrize("field,value,code", [
-    ("head_dim", 64, 2), ("group", 48, 2), ("hi_bits", 4, 2), ("lo_bits", 3, 2),
+    ("head_dim", 64, 2), ("group", 48, 2), ("hi_bits", 2, 2), ("lo_bits", 3, 2),
     ("q_heads", 6, 1), ("kv_heads", 0, 1), ("cap_hi", 0, 1), ("batch", 0, 1),
 ])
 def test_cache_validation_errors(field, value, code):
     c = _desc(**{field: value})
     assert _call_attention(c) == code
     assert mikv.lib().mikv_last_error()
+
+
+def test_int4_importance_pool_needs_two_bit_or_evicting_retained_pool():
+    assert _call_attention(_desc(hi_bits=4, lo_bits=4)) == 2
+    assert _call_attention(_desc(hi_bits=4, lo_bits=8)) == 2
 
 
 def test_two_bit_gqa_pool_capacity_multiple_of_32():

@@ -295,6 +295,34 @@ def test_lockstep_with_prompt_importance():
         run.step(t)
 
 
+@pytest.mark.parametrize("name", ["long_context", "llama2_13b", "mistral_7b"])
+@pytest.mark.parametrize("fused", [False, True])
+def test_lockstep_int4_importance_cache(name, fused):
+    """Table 3's INT4 importance cache over the 2-bit retained cache: MHA,
+    balanced (13B shape) and GQA, demotions re-quantizing decoded INT4 rows."""
+    _dev()
+    wl = workloads.small_workload(name, **SMALL[name], hi_bits=4, lo_bits=2)
+    run = Lockstep(wl, 4, fused=fused)
+    run.prefill()
+    for t in range(4):
+        run.step(t)
+
+
+def test_full_size_int4_importance_sampled_heads():
+    """The INT4 importance cache at the long_context size in the benchmark's
+    launch configuration, the oracle following three heads."""
+    _dev()
+    wl = workloads.WORKLOADS["long_context"].with_(hi_bits=4)
+    NH = wl.n_heads
+    print(f"[full-size int4 importance] long_context: {NH} heads, 2 steps", flush=True)
+    run = SampledLockstep(wl, 2, heads=[0, NH // 2 + 1, NH - 1])
+    run.prefill()
+    for t in range(2):
+        run.step(t)
+    del run
+    torch.cuda.empty_cache()
+
+
 def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
     dev = _dev()
     c = mikv.MikvCache(1, 2, 2, 32, 16, 2, cap_hi=4, cap_lo=32, max_len=64, device=dev)

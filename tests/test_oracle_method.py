@@ -321,6 +321,32 @@ def test_eviction_baseline_attends_to_the_kept_tokens_only():
         assert not (c.is_hi[:, :L] & ~attended).any()
 
 
+def test_int4_importance_cache_demotes_through_its_decoded_values():
+    """Table 3's INT4 importance cache: prompt tokens kept at high precision
+    hold Eq. 1 codes at 4 bits, and a token demoted to the 2-bit retained
+    cache is Eq. 1 at 2 bits of its decoded INT4 values."""
+    wl = workloads.WORKLOADS["tiny"]
+    wl, k, v, sc, q, kn, vn = _tiny_inputs(wl, 120, 3, seed=9)
+    c = oracle.OracleCache(wl.n_heads, 1, 130, 4, 2, 32)
+    kh0 = oracle.heavy_budget(120, 1, 5, 8, False)
+    c.prefill(k, v, sc, kh0, 8)
+    h, j = 0, int(np.nonzero(c.is_hi[0, :120])[0][0])
+    codes, a, b = oracle.quantize(k[h, j].astype(np.float32), 4, 32)
+    np.testing.assert_array_equal(c.hk[h, j], codes)
+    np.testing.assert_array_equal(c.hk_a[h, j], a)
+    assert int(c.hk[:, :120].max()) <= 15
+    for t in range(3):
+        before, hk, hka, hkb = c.is_hi.copy(), c.hk.copy(), c.hk_a.copy(), c.hk_b.copy()
+        L = 121 + t
+        c.step(q[t, 0][:, None].numpy(), kn[t, 0].numpy(), vn[t, 0].numpy(), SCALE,
+               oracle.heavy_budget(L, 1, 5, 8, False), 8)
+        before[:, L - 1] = True
+        for hh in range(wl.n_heads):
+            for jj in np.nonzero(before[hh, :L] & ~c.is_hi[hh, :L])[0]:
+                val = oracle.dequantize(hk[hh, jj], hka[hh, jj], hkb[hh, jj], 32)
+                np.testing.assert_array_equal(c.lk[hh, jj], oracle.quantize(val, 2, 32)[0])
+
+
 def test_step_invariants_and_demotion_path():
     wl = workloads.WORKLOADS["tiny"]
     wl, k, v, sc, q, kn, vn = _tiny_inputs(wl, 200, 6, seed=3)
