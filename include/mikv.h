@@ -104,7 +104,7 @@ typedef struct mikv_cache {
   int32_t head_dim;   /* 128 */
   int32_t group;      /* quantization group size: 32, 64 or 128 channels */
   int32_t hi_bits;    /* 16 (fp16), 8 (INT8) or 4 (INT4, with lo_bits 2 or 0) */
-  int32_t lo_bits;    /* 2, 4 or 8; 0 = evict instead of retaining (see above) */
+  int32_t lo_bits;    /* 2, 3 (q_heads / kv_heads <= 2), 4 or 8; 0 = evict instead of retaining (see above) */
   int32_t cap_hi;     /* importance-pool slots per head */
   int32_t cap_lo;     /* retained-pool slots per head (ignored when lo_bits is 0) */
   int32_t max_len;    /* positions per head (length of map rows) */
@@ -179,7 +179,7 @@ int mikv_prefill_importance(const uint16_t *q_prefill, const uint16_t *k_prefill
  *   x      fp16 [rows, 128];   balance fp32 [rows / rows_per_balance, 128] or NULL;
  *   codes  uint8 [rows, 128 * bits / 8] (packed, LSB first);
  *   params fp16 (alpha, beta) pairs [rows, 128 / group, 2].
- * bits in {2, 4, 8}; group in {32, 64, 128}.  rows == 0 is a no-op (pointers may
+ * bits in {2, 3, 4, 8} (3-bit codes straddle bytes); group in {32, 64, 128}.  rows == 0 is a no-op (pointers may
  * then be NULL).
  */
 int mikv_quantize_rows(const uint16_t *x, int64_t rows, int32_t head_dim, const float *balance,

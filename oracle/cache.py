@@ -40,7 +40,7 @@ class OracleCache:
 
     def __init__(self, n_heads: int, group_size: int, max_len: int, hi_bits: int, lo_bits: int,
                  group: int, head_dim: int = 128):
-        assert hi_bits in (16, 8, 4) and lo_bits in (0, 2, 4, 8)
+        assert hi_bits in (16, 8, 4) and lo_bits in (0, 2, 3, 4, 8)
         self.n_heads, self.G, self.max_len = n_heads, group_size, max_len
         self.hi_bits, self.lo_bits, self.group, self.d = hi_bits, lo_bits, group, head_dim
         ng = head_dim // group

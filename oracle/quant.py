@@ -74,24 +74,30 @@ def dequantize(codes, alpha16, beta16, group: int) -> np.ndarray:
 
 
 def pack(codes, bits: int) -> np.ndarray:
-    """Pack N-bit codes along the last axis, least significant bits first."""
+    """Pack N-bit codes along the last axis, least significant bits first:
+    code c occupies bits [N c, N c + N) of the row's bit string, bit b of the
+    string being bit b % 8 of byte b // 8 (so a 3-bit code may straddle two
+    bytes)."""
     codes = np.asarray(codes, dtype=np.uint8)
     *lead, d = codes.shape
-    per = 8 // bits
-    c = codes.reshape(*lead, d // per, per).astype(np.uint32)
-    out = np.zeros((*lead, d // per), dtype=np.uint32)
-    for i in range(per):
-        out |= c[..., i] << (bits * i)
-    return out.astype(np.uint8)
+    assert (d * bits) % 8 == 0
+    bitarr = np.zeros((*lead, d * bits), dtype=np.uint8)       # one entry per bit, LSB first
+    for i in range(bits):
+        bitarr[..., i::bits] = (codes >> i) & 1
+    weights = (1 << np.arange(8)).astype(np.uint32)
+    return (bitarr.reshape(*lead, d * bits // 8, 8).astype(np.uint32) * weights).sum(-1).astype(np.uint8)
 
 
 def unpack(packed, bits: int) -> np.ndarray:
     """Inverse of :func:`pack`."""
     packed = np.asarray(packed, dtype=np.uint8)
-    per = 8 // bits
-    mask = (1 << bits) - 1
-    parts = [(packed >> (bits * i)) & mask for i in range(per)]
-    return np.stack(parts, axis=-1).reshape(*packed.shape[:-1], packed.shape[-1] * per).astype(np.uint8)
+    *lead, nb = packed.shape
+    bitarr = ((packed[..., None] >> np.arange(8)) & 1).reshape(*lead, nb * 8)
+    d = nb * 8 // bits
+    out = np.zeros((*lead, d), dtype=np.uint32)
+    for i in range(bits):
+        out |= bitarr[..., i::bits][..., :d].astype(np.uint32) << i
+    return out.astype(np.uint8)
 
 
 def bits_per_element(bits: int, group: int) -> float:

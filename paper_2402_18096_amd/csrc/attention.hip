@@ -99,13 +99,13 @@ template <int BITS>
 struct Fmt {
   static constexpr bool kQuant = BITS != 16;
   __host__ __device__ static constexpr int lo(int p) {
-    return BITS == 16 ? 2 * p
+    return BITS == 16 || BITS == 3 ? 2 * p
          : BITS == 8  ? 4 * (p / 2) + p % 2
          : BITS == 4  ? 8 * (p / 4) + p % 4
                       : 16 * (p / 8) + p % 8;
   }
   __host__ __device__ static constexpr int hi(int p) {
-    return BITS == 16 ? 2 * p + 1 : lo(p) + (BITS == 8 ? 2 : BITS == 4 ? 4 : 8);
+    return BITS == 16 || BITS == 3 ? 2 * p + 1 : lo(p) + (BITS == 8 ? 2 : BITS == 4 ? 4 : 8);
   }
   __host__ __device__ static constexpr int cls(int p) {
     return BITS == 4 ? 4 * (p % 2) : BITS == 2 ? 2 * (p % 4) : 0;
@@ -115,6 +115,18 @@ struct Fmt {
     if constexpr (BITS == 16) {
 #pragma unroll
       for (int j = 0; j < CPL / 2; ++j) out[j] = raw[j];
+    } else if constexpr (BITS == 3) {
+      // 3-bit codes straddle bytes and words: each pair (channels 2j,
+      // 2j+1, bits 6j .. 6j+5 of the lane's 96) is extracted from the
+      // 64-bit window that holds it into the low bits of the two halves
+      static_assert(CPL == 32, "3-bit rows: 32 channels per lane");
+#pragma unroll
+      for (int j = 0; j < CPL / 2; ++j) {
+        const int bit = 6 * j, wi = bit / 32, sh = bit % 32;
+        const uint64_t win = ((uint64_t)(wi + 1 < 3 ? raw[wi + 1] : 0u) << 32) | raw[wi];
+        const uint32_t x = (uint32_t)(win >> sh);
+        out[j] = (x & 7u) | (((x >> 3) & 7u) << 16);
+      }
     } else if constexpr (BITS == 8) {
 #pragma unroll
       for (int j = 0; j < CPL / 4; ++j) {
@@ -208,6 +220,15 @@ __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, r
 #pragma unroll
         for (int j = 0; j < 4; ++j) r.v[4 * i + j] = b[j];
       }
+    }
+  } else if constexpr (KW == 3) {
+    if constexpr (LK) {
+      auto a = __builtin_amdgcn_raw_buffer_load_b96(rk, orow, 0, 0);
+      r.k[0] = a[0]; r.k[1] = a[1]; r.k[2] = a[2];
+    }
+    if constexpr (LV) {
+      auto b = __builtin_amdgcn_raw_buffer_load_b96(rv, orow, 0, 0);
+      r.v[0] = b[0]; r.v[1] = b[1]; r.v[2] = b[2];
     }
   } else if constexpr (KW == 2) {
     if constexpr (LK) {
@@ -1006,7 +1027,9 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #define MIKV_UNROLL_INT4 4
 #endif
 template <int BITS>
-constexpr int unroll_for() { return BITS == 4 ? MIKV_UNROLL_INT4 : BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL_HIGHBIT; }
+constexpr int unroll_for() {
+  return BITS == 4 || BITS == 3 ? MIKV_UNROLL_INT4 : BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL_HIGHBIT;
+}
 template <int BITS>
 constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PREFETCH_HIGHBIT; }
 
@@ -1077,6 +1100,9 @@ void attn_partial_kernel(AttnArgs A) {
       attn_chunk_int2<G, SPLITQ, 2>(A, h, c - A.nc_hi, c, s_lds, w_lds);
     else
       attn_chunk_int2<G, SPLITQ, 1>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+  } else if constexpr (LO == 3 && CPL != 32) {
+    // not reached: the host rejects 3-bit retained pools above two query
+    // heads per KV head
   } else {
     attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
   }
@@ -1543,6 +1569,8 @@ int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const
     case 1604: launch_partial_g<16, 4>(A, G, grid, st); break;
     case 1608: launch_partial_g<16, 8>(A, G, grid, st); break;
     case 802: launch_partial_g<8, 2>(A, G, grid, st); break;
+    case 1603: launch_partial_g<16, 3>(A, G, grid, st); break;
+    case 803: launch_partial_g<8, 3>(A, G, grid, st); break;
     case 402: launch_partial_g<4, 2>(A, G, grid, st); break;
     case 804: launch_partial_g<8, 4>(A, G, grid, st); break;
     default: launch_partial_g<8, 8>(A, G, grid, st); break;
@@ -1581,6 +1609,8 @@ int decode_finalize_select(const mikv_cache *c, int32_t length, const uint16_t *
     case 1604: launch_finalize_select<16, 4>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 1608: launch_finalize_select<16, 8>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 802: launch_finalize_select<8, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    case 1603: launch_finalize_select<16, 3>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
+    case 803: launch_finalize_select<8, 3>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 402: launch_finalize_select<4, 2>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     case 804: launch_finalize_select<8, 4>(A, S, G, grid, tiles_hi, tiles_lo, st); break;
     default: launch_finalize_select<8, 8>(A, S, G, grid, tiles_hi, tiles_lo, st); break;

@@ -139,6 +139,16 @@ __device__ inline uint32_t encode(float x, const GroupParams &p, int bits) {
   return (uint32_t)t;
 }
 
+// Put code `v` of channel c (of a lane's 32) into the packed little-endian
+// words w[BITS], least significant bits first; a 3-bit code can straddle two
+// words.
+template <int BITS>
+__device__ inline void put_code(uint32_t w[BITS], int c, uint32_t v) {
+  const int bit = c * BITS, wi = bit / 32, sh = bit % 32;
+  w[wi] |= v << sh;
+  if (sh + BITS > 32) w[wi + 1] |= v >> (32 - sh);
+}
+
 // encode() of the 32 values of one lane's segment, packed LSB-first into
 // w[BITS], without a divide per value: the quotient (x - beta) / alpha is
 // estimated as (x - beta) * fl(1 / alpha), within 1.5 ulp of the correctly
@@ -166,8 +176,7 @@ __device__ inline void encode32(const float x[32], const GroupParams &p, uint32_
 #pragma unroll
   for (int i = 0; i < BITS; ++i) w[i] = 0u;
 #pragma unroll
-  for (int c = 0; c < 32; ++c)
-    w[(c * BITS) / 32] |= (uint32_t)fminf(fmaxf(rintf(q[c]), 0.0f), top) << ((c * BITS) % 32);
+  for (int c = 0; c < 32; ++c) put_code<BITS>(w, c, (uint32_t)fminf(fmaxf(rintf(q[c]), 0.0f), top));
 }
 
 // c ? a : b for wave-uniform pointers (argument fields) and a per-lane

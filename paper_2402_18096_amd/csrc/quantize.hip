@@ -334,8 +334,8 @@ extern "C" int mikv_quantize_rows(const uint16_t *x, int64_t rows, int32_t head_
   if (rows == 0) return MIKV_OK;  // nothing to do; pointers may be NULL
   if (!x || !codes || !params) return set_error(MIKV_ERR_INVALID_ARG, "mikv_quantize_rows: NULL pointer");
   if (head_dim != kHeadDim) return set_error(MIKV_ERR_UNSUPPORTED, "mikv_quantize_rows: head_dim must be 128");
-  if (bits != 2 && bits != 4 && bits != 8)
-    return set_error(MIKV_ERR_UNSUPPORTED, "mikv_quantize_rows: bits must be 2, 4 or 8");
+  if (bits != 2 && bits != 3 && bits != 4 && bits != 8)
+    return set_error(MIKV_ERR_UNSUPPORTED, "mikv_quantize_rows: bits must be 2, 3, 4 or 8");
   if (group != 32 && group != 64 && group != 128)
     return set_error(MIKV_ERR_UNSUPPORTED, "mikv_quantize_rows: group must be 32, 64 or 128");
   if (balance && rows_per_balance < 1)
@@ -346,6 +346,10 @@ extern "C" int mikv_quantize_rows(const uint16_t *x, int64_t rows, int32_t head_
   switch (bits) {
     case 2:
       hipLaunchKernelGGL(quantize_rows_kernel<2>, grid, dim3(256), 0, st, x, rows, balance, rows_per_balance,
+                         group, codes, params);
+      break;
+    case 3:
+      hipLaunchKernelGGL(quantize_rows_kernel<3>, grid, dim3(256), 0, st, x, rows, balance, rows_per_balance,
                          group, codes, params);
       break;
     case 4:
@@ -387,6 +391,8 @@ extern "C" int mikv_quantize_kv(const mikv_cache *c, const uint16_t *k, const ui
     case 1604: launch_place<16, 4>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 1608: launch_place<16, 8>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 802: launch_place<8, 2>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
+    case 1603: launch_place<16, 3>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
+    case 803: launch_place<8, 3>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 402: launch_place<4, 2>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     case 804: launch_place<8, 4>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     default: launch_place<8, 8>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;

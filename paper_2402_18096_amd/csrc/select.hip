@@ -73,6 +73,8 @@ int select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t wi
     case 1604: launch_select<16, 4>(A, NH, st); break;
     case 1608: launch_select<16, 8>(A, NH, st); break;
     case 802: launch_select<8, 2>(A, NH, st); break;
+    case 1603: launch_select<16, 3>(A, NH, st); break;
+    case 803: launch_select<8, 3>(A, NH, st); break;
     case 402: launch_select<4, 2>(A, NH, st); break;
     case 804: launch_select<8, 4>(A, NH, st); break;
     default: launch_select<8, 8>(A, NH, st); break;

@@ -194,7 +194,7 @@ __device__ inline GroupParams lo_words(const SelArgs &A, const float x[32], uint
 #pragma unroll
   for (int i = 0; i < LO_BITS; ++i) w[i] = 0u;
 #pragma unroll
-  for (int c = 0; c < 32; ++c) w[(c * LO_BITS) / 32] |= encode(x[c], p, LO_BITS) << ((c * LO_BITS) % 32);
+  for (int c = 0; c < 32; ++c) put_code<LO_BITS>(w, c, encode(x[c], p, LO_BITS));
   return p;
 }
 

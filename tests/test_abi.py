@@ -49,13 +49,17 @@ def _call_attention(c, length=4, ws_bytes=1 << 30):
 
 
 @pytest.mark.parametrize("field,value,code", [
-    ("head_dim", 64, 2), ("group", 48, 2), ("hi_bits", 2, 2), ("lo_bits", 3, 2),
+    ("head_dim", 64, 2), ("group", 48, 2), ("hi_bits", 2, 2), ("lo_bits", 5, 2),
     ("q_heads", 6, 1), ("kv_heads", 0, 1), ("cap_hi", 0, 1), ("batch", 0, 1),
 ])
 def test_cache_validation_errors(field, value, code):
     c = _desc(**{field: value})
     assert _call_attention(c) == code
     assert mikv.lib().mikv_last_error()
+
+
+def test_three_bit_retained_pool_at_most_two_query_heads_per_kv_head():
+    assert _call_attention(_desc(lo_bits=3, q_heads=4, kv_heads=1)) == 2
 
 
 def test_int4_importance_pool_needs_two_bit_or_evicting_retained_pool():
@@ -87,7 +91,7 @@ def test_null_pointers_and_capacity():
     assert _call_attention(c, length=17) == 3        # length > max_len
     assert _call_attention(c, ws_bytes=16) == 3      # workspace too small
     assert L.mikv_quantize_rows(None, 4, 128, None, 1, 2, 32, None, None, None) == 1
-    assert L.mikv_quantize_rows(ctypes.c_void_p(1), 4, 128, None, 1, 3, 32, ctypes.c_void_p(1),
+    assert L.mikv_quantize_rows(ctypes.c_void_p(1), 4, 128, None, 1, 5, 32, ctypes.c_void_p(1),
                                 ctypes.c_void_p(1), None) == 2
     assert L.mikv_select_topk(ctypes.byref(_desc()), 4, -1, 0, ctypes.c_void_p(1), 1 << 20, None) == 1
     assert L.mikv_select_prefill(None, 1, 4, 1, 1, None, None) == 1

@@ -37,7 +37,7 @@ def _adversarial_rows(rng, rows, bits, group):
     return x.astype(np.float16)
 
 
-@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
 @pytest.mark.parametrize("group", [32, 64, 128])
 @pytest.mark.parametrize("balanced", [False, True])
 def test_quantize_rows_bit_exact(bits, group, balanced):
@@ -315,6 +315,38 @@ def test_full_size_int4_importance_sampled_heads():
     wl = workloads.WORKLOADS["long_context"].with_(hi_bits=4)
     NH = wl.n_heads
     print(f"[full-size int4 importance] long_context: {NH} heads, 2 steps", flush=True)
+    run = SampledLockstep(wl, 2, heads=[0, NH // 2 + 1, NH - 1])
+    run.prefill()
+    for t in range(2):
+        run.step(t)
+    del run
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,extra", [
+    ("long_context", {}),
+    ("llama2_13b", {}),                                   # balanced INT8 importance pool
+    ("mistral_7b", dict(q_heads=4, kv_heads=2)),          # two query heads per KV head
+])
+@pytest.mark.parametrize("fused", [False, True])
+def test_lockstep_int3_retained_cache(name, extra, fused):
+    """The INT3 retained cache of Tables 1 and 2 (codes straddling bytes):
+    prefill, attention, demotion and re-quantization, bit-exact state."""
+    _dev()
+    wl = workloads.small_workload(name, **{**SMALL[name], **extra}, lo_bits=3)
+    run = Lockstep(wl, 4, fused=fused)
+    run.prefill()
+    for t in range(4):
+        run.step(t)
+
+
+def test_full_size_int3_retained_sampled_heads():
+    """The INT3 retained cache at the long_context size in the benchmark's
+    launch configuration, the oracle following three heads."""
+    _dev()
+    wl = workloads.WORKLOADS["long_context"].with_(lo_bits=3)
+    NH = wl.n_heads
+    print(f"[full-size int3 retained] long_context: {NH} heads, 2 steps", flush=True)
     run = SampledLockstep(wl, 2, heads=[0, NH // 2 + 1, NH - 1])
     run.prefill()
     for t in range(2):

@@ -69,7 +69,7 @@ def _random_groups(rng, n, g, scale=1.0):
     return x
 
 
-@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
 @pytest.mark.parametrize("g", [32, 64])
 def test_nearest_level_brute_force(bits, g):
     """Each code names the level alpha*c + beta nearest to x (up to fp32
@@ -90,7 +90,7 @@ def test_nearest_level_brute_force(bits, g):
     assert c.max() <= 2 ** bits - 1
 
 
-@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
 def test_reconstruction_error_bound(bits):
     """|x - x_hat| <= alpha/2 + |beta16 - min| + |alpha16*(2^N-1) - range| + fp32 slack."""
     g = 32
@@ -182,7 +182,7 @@ def test_memory_table_head_shapes():
     assert round(gb(32, 32) * 0.25, 2) == 8.59 and round(gb(32, 32) * 0.2, 2) == 6.87
 
 
-@pytest.mark.parametrize("bits", [2, 4, 8])
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
 def test_exact_quotient_ties_round_half_even(bits):
     """Eq. 1 on groups whose quotients (x - beta) / alpha are exact
     half-integers or one fp16 ulp from them: every code is the quotient taken
@@ -202,3 +202,20 @@ def test_exact_quotient_ties_round_half_even(bits):
             ties += q.denominator == 2
             assert int(c[r, j]) == min(max(round(q), 0), top), (r, j, q)
     assert ties > x.size // 3
+
+
+def test_three_bit_packing_straddles_bytes():
+    """3-bit codes packed least significant bits first across byte
+    boundaries: the row's bit string read as one little-endian integer is
+    sum_c code_c * 8**c (big-integer arithmetic, independent of the packer)."""
+    rng = np.random.default_rng(7)
+    codes = rng.integers(0, 8, size=(3, 128)).astype(np.uint8)
+    packed = oracle.pack(codes, 3)
+    assert packed.shape == (3, 48)
+    for r in range(3):
+        value = sum(int(c) << (3 * i) for i, c in enumerate(codes[r]))
+        np.testing.assert_array_equal(packed[r], np.frombuffer(value.to_bytes(48, "little"), np.uint8))
+    np.testing.assert_array_equal(oracle.unpack(packed, 3), codes)
+    # the first eight codes 1..7, 0 give the 24-bit word 0x1F58D1
+    first = np.array([[1, 2, 3, 4, 5, 6, 7, 0]], np.uint8)
+    np.testing.assert_array_equal(oracle.pack(first, 3)[0], [0xD1, 0x58, 0x1F])
