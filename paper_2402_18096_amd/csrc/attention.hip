@@ -81,6 +81,7 @@ struct AttnArgs {
   // non-NULL) and n_hi does not count it until the re-rank writes it.
   AppendArgs app;
   int hi_pending;
+  int pool_major;  // dispatch every importance-pool chunk first (fp16 importance pools)
 };
 
 // Importance-pool tokens of head h, the pending new token included.
@@ -1074,13 +1075,23 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_P
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
   // Block -> (head, chunk): first every head's importance-pool chunks and
-  // the retained-pool chunks that cannot be empty (nc_first per head), then
+  // the retained-pool chunks that cannot be empty (nc_first per head; with
+  // pool_major all importance-pool chunks, the longest-running waves of an
+  // fp16 pool, before any retained-pool chunk), then
   // the retained-pool chunks that may be (a wave that finds its chunk empty
   // costs little at the end of the grid, but holds up the dispatch of the
   // work behind it anywhere else).
-  const int n_first = gridDim.x / (A.nc_hi + A.nc_lo) * A.nc_first;  // blocks of the first part
+  const int n_heads = gridDim.x / (A.nc_hi + A.nc_lo);
+  const int n_first = n_heads * A.nc_first;  // blocks of the first part
   int h, c;
-  if ((int)blockIdx.x < n_first) {
+  if (A.pool_major && (int)blockIdx.x < n_heads * A.nc_hi) {
+    h = blockIdx.x / A.nc_hi;
+    c = blockIdx.x % A.nc_hi;
+  } else if (A.pool_major && (int)blockIdx.x < n_first) {
+    const int e = blockIdx.x - n_heads * A.nc_hi, per = A.nc_first - A.nc_hi;
+    h = e / per;
+    c = A.nc_hi + e % per;
+  } else if ((int)blockIdx.x < n_first) {
     h = blockIdx.x / A.nc_first;
     c = blockIdx.x % A.nc_first;
   } else {
@@ -1479,6 +1490,10 @@ AttnArgs make_args(const mikv_cache *c, const Plan &p, const uint16_t *q, const 
   A.nc_first = p.nc_first;
   A.app = AppendArgs{};
   A.hi_pending = 0;
+  // fp16 importance-pool chunks run longest: dispatched first, the tail of
+  // the grid is shorter (measured: long_context -1.8 %, mistral_7b -2.3 % per
+  // step; an INT8 pool gained nothing, llama2_7b lost 1.2 %)
+  A.pool_major = c->hi_bits == 16 ? 1 : 0;
   return A;
 }
 
