@@ -1043,7 +1043,10 @@ constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PR
 #define MIKV_WAVES_PER_EU 1
 #endif
 #ifndef MIKV_CHUNK_KB
-#define MIKV_CHUNK_KB 96
+#define MIKV_CHUNK_KB 96  // under GQA
+#endif
+#ifndef MIKV_CHUNK_KB_MHA
+#define MIKV_CHUNK_KB_MHA 64  // one query head per KV head (measured: 13B shape -2.5 %, long_context even)
 #endif
 #ifndef MIKV_CHUNK_HI_SCALE
 #define MIKV_CHUNK_HI_SCALE 2  // MHA importance-pool chunks hold this many times the bytes
@@ -1427,10 +1430,12 @@ Plan make_plan(const mikv_cache *c, int length) {
   const int span_hi = std::min(length, c->cap_hi), span_lo = evicting(c) ? 0 : std::min(length, c->cap_lo);
   const int64_t bh = token_bytes(c->hi_bits, c->group), bl = token_bytes(evicting(c) ? 2 : c->lo_bits, c->group);
   const int64_t total = NH * (span_hi * bh + span_lo * bl);
-  // One wave per chunk; up to 96 KiB of packed K/V per chunk (many small work
-  // units balance the CUs best), at least 16 KiB so the per-chunk merge
-  // stays cheap.  Chunks are whole wave iterations (128 tokens).
-  int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, MIKV_CHUNK_KB << 10), 16 << 10);
+  // One wave per chunk; up to 64 KiB (MHA) or 96 KiB (GQA) of packed K/V per
+  // chunk (many small work units balance the CUs best), at least 16 KiB so
+  // the per-chunk merge stays cheap.  Chunks are whole wave iterations (128
+  // tokens).
+  const int64_t chunk_kb = group_size_of(c) == 1 ? MIKV_CHUNK_KB_MHA : MIKV_CHUNK_KB;
+  int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, chunk_kb << 10), 16 << 10);
   const int cmax = max_chunk(group_size_of(c));
   // MHA importance-pool rows cost the least work per byte: twice the bytes
   // per chunk there halve the per-wave overhead (measured: 4 % of the
