@@ -4,9 +4,9 @@
  * Mixed Precision Quantization", arXiv 2402.18096) for AMD MI355X (gfx950).
  *
  * A MiKV cache keeps, per (sequence, KV head), the tokens ranked important
- * by accumulated attention at high precision (fp16 or INT8: the "importance
- * cache") and every other token at low precision (INT4/INT2, per-token
- * grouped asymmetric: the "retained cache") instead of evicting it
+ * by accumulated attention at high precision (fp16, INT8 or INT4: the
+ * "importance cache") and every other token at low precision (INT4/INT3/INT2,
+ * per-token grouped asymmetric: the "retained cache") instead of evicting it
  * (Section 3, Fig. 3).  Because attention after RoPE is permutation
  * invariant, the two precisions are stored as two separate pools (Section
  * 3.4); a token's position travels with it in a position array.
@@ -200,7 +200,8 @@ int mikv_quantize_rows(const uint16_t *x, int64_t rows, int32_t head_dim, const 
  * Tokens are appended to their pool after the occupied slots, in position
  * order; hi_pos/lo_pos, n_hi/n_lo, hi_acc and map are updated.  Importance
  * tokens are stored as fp16 (hi_bits 16: fp16 of the fp32 balanced key) or
- * INT8 codes, retained tokens as lo_bits codes.
+ * INT8/INT4 codes, retained tokens as lo_bits codes (dropped when lo_bits is
+ * 0).
  *   workspace: at least mikv_quantize_workspace_size(c, n) bytes (0 when
  *   hi_mask is NULL).
  * Errors: INVALID_ARG (null pointers, n < 1, pos0 < 0), CAPACITY (pos0 + n >
@@ -264,9 +265,10 @@ int mikv_importance_update(const mikv_cache *c, int32_t length, const float *pro
  * window is positions [length - window, length); eligible tokens are the
  * importance-pool tokens outside the window.  The k_heavy eligible tokens
  * with the largest key (score, position) stay; every other eligible token is
- * demoted: its stored high-precision key/value (fp16, or INT8 decoded in
- * fp32) is re-quantized with Eq. 1 at lo_bits into the retained pool (keys
- * are already balanced), its map entry set to 0, and its importance slot is
+ * demoted: its stored high-precision key/value (fp16, or INT8/INT4 decoded
+ * in fp32) is re-quantized with Eq. 1 at lo_bits into the retained pool
+ * (keys are already balanced; with lo_bits 0 it is dropped instead), its
+ * map entry set to 0, and its importance slot is
  * refilled from the end of the pool.  Demotion is one way.
  *   workspace at least mikv_select_workspace_size(c) bytes.
  * Errors: INVALID_ARG (k_heavy < 0, window < 0, length > max_len), CAPACITY.

@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(const uint16_t *x, i
 
 // Device view of the cache for the placement kernels.
 struct Pools {
-  uint8_t *hi_k, *hi_v;      // fp16 or INT8 codes
+  uint8_t *hi_k, *hi_v;      // fp16 rows, or INT8/INT4 codes
   uint32_t *hi_kp, *hi_vp;   // (alpha, beta) pairs
   int32_t *hi_pos;
   float *hi_acc;
