@@ -295,7 +295,7 @@ def test_lockstep_with_prompt_importance():
         run.step(t)
 
 
-@pytest.mark.parametrize("name", ["long_context", "llama2_13b", "mistral_7b"])
+@pytest.mark.parametrize("name", ["long_context", "llama2_7b", "llama2_13b", "mistral_7b"])
 @pytest.mark.parametrize("fused", [False, True])
 def test_lockstep_int4_importance_cache(name, fused):
     """Table 3's INT4 importance cache over the 2-bit retained cache: MHA,
@@ -325,6 +325,7 @@ def test_full_size_int4_importance_sampled_heads():
 
 @pytest.mark.parametrize("name,extra", [
     ("long_context", {}),
+    ("llama2_7b", {}),                                    # INT8 importance pool, group 64
     ("llama2_13b", {}),                                   # balanced INT8 importance pool
     ("mistral_7b", dict(q_heads=4, kv_heads=2)),          # two query heads per KV head
 ])
