@@ -209,6 +209,16 @@ def test_lockstep_eviction(name, fused):
         run.step(t)
 
 
+def test_lockstep_eviction_with_int4_importance_cache():
+    """Eviction with an INT4 importance cache (hi_bits 4, lo_bits 0), GQA."""
+    _dev()
+    wl = workloads.small_workload("mistral_7b", **SMALL["mistral_7b"], hi_bits=4, lo_bits=0)
+    run = Lockstep(wl, 3, fused=True)
+    run.prefill()
+    for t in range(3):
+        run.step(t)
+
+
 def test_lockstep_eviction_many_demotions():
     """Several evictions per head and step (the radix-select path)."""
     _dev()
