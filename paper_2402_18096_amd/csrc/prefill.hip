@@ -8,11 +8,13 @@
 // on the matrix cores (v_mfma_f32_16x16x32_f16, fp16 operands as given,
 // fp32 accumulation):
 //   pass 1  one wave per 64 queries of one query head: online row maximum
-//           and normaliser over the causal keys, in log2 units;
+//           (raised lazily) and normaliser over the causal keys, in log2 units;
 //   pass 2  one wave per 64 keys of one KV head: recomputes the same 16x16
 //           logit tiles (bit-identical: same operands, same tile origin),
 //           turns them into probabilities with the pass-1 statistics and
 //           sums them down the columns, over every query head of the group.
+// Tiles entirely below the causal diagonal and inside the prompt (nearly
+// all of them) skip the mask.
 // Lane l = 16 a + n of a wave: A operand = rows n of the query tile, B
 // operand = rows n of the key tile, each lane taking channels
 // [32 c + 8 a, 32 c + 8 a + 8) of MFMA c (the same split on both sides, so
@@ -26,6 +28,7 @@ namespace {
 
 constexpr int kTileBlocks = 4;  // 16-row tiles per wave in each pass (64 rows)
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLazy = 8.0f;   // raise a row's running maximum only past this (log2 units)
 
 typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
 typedef float f4_t __attribute__((ext_vector_type(4)));
@@ -72,6 +75,10 @@ __global__ __launch_bounds__(64) void prefill_rowstats_kernel(const uint16_t *q,
   uint4 aq[kTileBlocks][4];
 #pragma unroll
   for (int rb = 0; rb < kTileBlocks; ++rb) load_rows(qb, i_base + 16 * rb + n, T, a, aq[rb]);
+  // Lazy row maximum (log2 units, the same in the 16 lanes of a row): raised
+  // only when a logit exceeds it by more than kLazy, decided for the whole
+  // wave with one ballot, so the common tile needs no cross-lane reduction;
+  // each lane sums its own exp2 terms, reduced once at the end.
   float m[kTileBlocks][4], l[kTileBlocks][4];
 #pragma unroll
   for (int rb = 0; rb < kTileBlocks; ++rb)
@@ -89,20 +96,34 @@ __global__ __launch_bounds__(64) void prefill_rowstats_kernel(const uint16_t *q,
     for (int rb = 0; rb < kTileBlocks; ++rb) {
       if (j0 > i_base + 16 * rb + 15) continue;  // tile above the diagonal (wave-uniform)
       const f4_t d = logits(aq[rb], bk);
+      // a tile below the diagonal and inside the prompt needs no mask
+      const bool full = j0 + 15 <= i_base + 16 * rb && i_base + 16 * rb + 15 < T;  // wave-uniform
+      float s[4];
+      bool raise = false;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int qi = i_base + 16 * rb + 4 * a + r;
-        const bool valid = kj <= qi && qi < T;
-        const float s = valid ? d[r] * s2scale : -__builtin_huge_valf();
-        const float mn = fmaxf(m[rb][r], max16(s));
-        if (mn == -__builtin_huge_valf()) continue;  // nothing valid in this row yet (row-uniform)
-        const float e = valid ? __builtin_amdgcn_exp2f(s - mn) : 0.0f;
-        const float f = m[rb][r] == -__builtin_huge_valf() ? 0.0f : __builtin_amdgcn_exp2f(m[rb][r] - mn);
-        l[rb][r] = fmaf(l[rb][r], f, sum16(e));
-        m[rb][r] = mn;
+        s[r] = full || (kj <= qi && qi < T) ? d[r] * s2scale : -__builtin_huge_valf();
+        raise = raise || s[r] > m[rb][r] + kLazy;
       }
+      if (__ballot(raise)) {  // wave-uniform
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float mn = fmaxf(m[rb][r], max16(s[r]));
+          if (mn != m[rb][r]) {  // row-uniform; mn is finite here
+            l[rb][r] *= m[rb][r] == -__builtin_huge_valf() ? 0.0f : __builtin_amdgcn_exp2f(m[rb][r] - mn);
+            m[rb][r] = mn;
+          }
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) l[rb][r] += s[r] == -__builtin_huge_valf() ? 0.0f : __builtin_amdgcn_exp2f(s[r] - m[rb][r]);
     }
   }
+#pragma unroll
+  for (int rb = 0; rb < kTileBlocks; ++rb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) l[rb][r] = sum16(l[rb][r]);
   if (n == 0) {
 #pragma unroll
     for (int rb = 0; rb < kTileBlocks; ++rb)
@@ -149,12 +170,21 @@ __global__ __launch_bounds__(64) void prefill_colsum_kernel(const uint16_t *q, c
         if (j_base + 16 * cb > i0 + 15) continue;  // tile above the diagonal (wave-uniform)
         const f4_t d = logits(aq, bk[cb]);
         const int kj = j_base + 16 * cb + n;
+        // a tile below the diagonal and inside the prompt needs no mask;
+        // the exponent is one fused multiply-add (within an ulp of pass 1's)
+        const bool full = j_base + 16 * cb + 15 <= i0 && i0 + 15 < T;  // wave-uniform
+        if (full) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int qi = i0 + 4 * a + r;
-          const bool valid = kj <= qi && qi < T;
-          const float p = __builtin_amdgcn_exp2f(d[r] * s2scale - ml[r].x) * ml[r].y;
-          cs[cb] += valid ? p : 0.0f;
+          for (int r = 0; r < 4; ++r)
+            cs[cb] = fmaf(__builtin_amdgcn_exp2f(fmaf(d[r], s2scale, -ml[r].x)), ml[r].y, cs[cb]);
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int qi = i0 + 4 * a + r;
+            const bool valid = kj <= qi && qi < T;
+            const float p = __builtin_amdgcn_exp2f(fmaf(d[r], s2scale, -ml[r].x)) * ml[r].y;
+            cs[cb] += valid ? p : 0.0f;
+          }
         }
       }
     }
