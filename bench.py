@@ -16,6 +16,8 @@ before the timed region starts.  Prints ONE JSON line on stdout:
              bytes per launch (the packed K/V bytes) / its mean duration from
              HIP events recorded on its stream, against 8 TB/s;
   cpu_baseline  the CPU oracle timed on a bounded sample of the same workload;
+  secondary  the same fields for a second workload (default llama2_13b, the
+             largest cache by bytes) timed in the same run;
   mall       untimed diagnostic: event-bracketed whole steps with warm caches
              and with the 256 MB last-level cache flushed before each step.
 
@@ -52,10 +54,14 @@ def track_counts(dec, n_hi, length):
 
 def cpu_baseline(wl, steps_inputs, budget_s: float):
     """The oracle, as it is, on a bounded sample: up to eight (sequence, KV
-    head) pairs of batch element 0, decode steps until the time budget is
-    used."""
+    head) pairs of batch element 0, decode steps from the end of prefill
+    until the time budget is used -- once with the BLAS threads the process
+    has, then, from a copy of the same prefilled cache, on one thread (half
+    the budget).  Both legs start at the first decode step, so each times
+    the same work per step; a leg that completes no step is an error."""
+    import copy
+
     import numpy as np
-    import torch
 
     import oracle
     from paper_2402_18096_amd import workloads
@@ -68,44 +74,56 @@ def cpu_baseline(wl, steps_inputs, budget_s: float):
     sc = workloads.initial_scores(wl, "cpu")[0].numpy()
     f16 = lambda t: t.detach().cpu().contiguous().numpy().view(np.float16)
     kk, vv = f16(k[0])[heads], f16(v[0])[heads]
+    del k, v
     bal = None
     if wl.balanced:
         qp = f16(workloads.prefill_queries(wl, q.device, batches=range(1))[0])
         qp = qp.reshape(wl.kv_heads, G, T, 128)[heads]
         bal = oracle.balancer(qp, kk)
     n_steps = q.shape[0]
-    orc = oracle.OracleCache(len(heads), G, T + n_steps, wl.hi_bits, wl.lo_bits, wl.group)
-    orc.prefill(kk, vv, sc[heads], oracle.heavy_budget(T, wl.ratio_num, wl.ratio_den, wl.window,
-                                                       wl.window_in_ratio), wl.window, bal)
+    orc0 = oracle.OracleCache(len(heads), G, T + n_steps, wl.hi_bits, wl.lo_bits, wl.group)
+    orc0.prefill(kk, vv, sc[heads], oracle.heavy_budget(T, wl.ratio_num, wl.ratio_den, wl.window,
+                                                        wl.window_in_ratio), wl.window, bal)
     qh = [h * G + i for h in heads for i in range(G)]
     tb = lambda bits: 0 if bits == 0 else 4 * 128 if bits == 16 else 2 * (128 * bits // 8 + 4 * (128 // wl.group))
+    # decode inputs of the sampled heads, on the host before any timing
+    qs = [f16(q[t, 0])[qh].reshape(len(heads), G, 128) for t in range(n_steps)]
+    ks = [f16(kn[t, 0])[heads] for t in range(n_steps)]
+    vs = [f16(vn[t, 0])[heads] for t in range(n_steps)]
 
-    def run(budget, first):
+    def run(orc, budget):
         done, nbytes, t0 = 0, 0, time.perf_counter()
-        while first + done < n_steps and time.perf_counter() - t0 < budget:
-            t = first + done
+        while done < n_steps and time.perf_counter() - t0 < budget:
             L = orc.length + 1
             n_hi = int(orc.is_hi[:, :L - 1].sum()) + len(heads)
             nbytes += n_hi * tb(wl.hi_bits) + (len(heads) * L - n_hi) * tb(wl.lo_bits)
-            orc.step(f16(q[t, 0])[qh].reshape(len(heads), G, 128), f16(kn[t, 0])[heads], f16(vn[t, 0])[heads],
-                     1.0 / math.sqrt(128.0),
+            orc.step(qs[done], ks[done], vs[done], 1.0 / math.sqrt(128.0),
                      oracle.heavy_budget(L, wl.ratio_num, wl.ratio_den, wl.window, wl.window_in_ratio), wl.window,
                      bal)
             done += 1
-        return done, nbytes, time.perf_counter() - t0
+        el = time.perf_counter() - t0
+        if done == 0:
+            raise RuntimeError(f"cpu baseline: no decode step completed within {budget:.1f} s")
+        return done, nbytes, el
 
-    done, nbytes, el = run(budget_s, 0)
+    orc1 = copy.deepcopy(orc0)
+    done, nbytes, el = run(orc0, budget_s)
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    # the same oracle on one thread, continuing the same decode, for a third of the budget
+    try:
+        host_cpus = len(os.sched_getaffinity(0))
+    except AttributeError:
+        host_cpus = os.cpu_count() or 1
     with threadpool_limits(limits=1):
-        done1, nbytes1, el1 = run(budget_s / 3, done)
-    return {"value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{len(heads)} of {wl.n_heads} (sequence, KV head) pairs x {done} decode steps "
+        done1, nbytes1, el1 = run(orc1, budget_s / 2)
+    return {"value": round(nbytes / el / 1e9, 4), "unit": "GB/s", "cores": int(min(threads, host_cpus)),
+            "kind": "oracle", "host_cpus": int(host_cpus), "host_cpu_count": os.cpu_count(),
+            "sample": f"{len(heads)} of {wl.n_heads} (sequence, KV head) pairs x the first {done} decode steps "
                       f"({el:.1f} s); numpy oracle, BLAS threads = {threads}",
-            "s_per_step_per_head": round(el / max(done, 1) / len(heads), 4),
-            "single_thread": {"value": round(nbytes1 / max(el1, 1e-9) / 1e9, 4), "unit": "GB/s", "cores": 1,
-                              "sample": f"the next {done1} decode steps of the same pairs ({el1:.1f} s), "
-                                        "BLAS limited to one thread"}}
+            "s_per_step_per_head": round(el / done / len(heads), 4),
+            "single_thread": {"value": round(nbytes1 / el1 / 1e9, 4), "unit": "GB/s", "cores": 1,
+                              "sample": f"the same pairs x the first {done1} decode steps ({el1:.1f} s), "
+                                        "BLAS limited to one thread",
+                              "s_per_step_per_head": round(el1 / done1 / len(heads), 4)}}
 
 
 # The attention partial kernel's source files (its traffic record is keyed by them).
@@ -209,14 +227,192 @@ def prefill_importance_probe(workload: str, reps: int):
     print(json.dumps(rec), flush=True)
 
 
+def apply_overrides(wl, overrides):
+    for ov in overrides:
+        key, val = ov.split("=", 1)
+        cur = getattr(wl, key)
+        wl = wl.with_(**{key: type(cur)(val) if not isinstance(cur, bool) else val in ("1", "true", "True")})
+    return wl
+
+
+def run_workload(wl, args, steps: int, warmup: int, cpu_seconds: float, overridden: bool):
+    """Prefill, warm up, time `steps` whole decode steps, then the untimed
+    diagnostic passes and the CPU baseline.  Returns the record's fields."""
+    import torch
+
+    from paper_2402_18096_amd import mikv, workloads
+
+    dev = torch.device("cuda:0")
+    n_total = warmup + steps + args.phase_steps + 2 * args.mall_steps
+    t_setup = time.perf_counter()
+    dec = mikv.MikvDecoder(wl, max_len=wl.context + n_total, device=dev, fused=bool(args.fused))
+    k, v = workloads.prefill_kv(wl, dev)
+    sc = workloads.initial_scores(wl, dev)
+    qp = workloads.prefill_queries(wl, dev) if wl.balanced else None
+    steps_inputs = workloads.decode_inputs(wl, n_total, dev)
+    q, kn, vn = steps_inputs
+    dec.prefill(k, v, sc, qp)
+    del k, v, qp
+    torch.cuda.synchronize()
+    log(f"[bench] {wl.name}: prefill of {wl.context} tokens x {wl.n_heads} heads done "
+        f"({time.perf_counter() - t_setup:.1f} s); warmup {warmup}, timed {steps}")
+
+    for t in range(warmup):
+        dec.step_native(q[t], kn[t], vn[t])
+    torch.cuda.synchronize()
+
+    n_hi = int(dec.cache.n_hi[0].item())
+    length = dec.length
+    step_bytes = []
+    for _ in range(steps):
+        length, n_attn, n_hi = track_counts(dec, n_hi, length)
+        step_bytes.append(dec.cache.packed_bytes(length, n_attn))
+
+    def fresh_events(n):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in evs:
+            e.record()
+        return evs
+
+    # Timed steps: two events per step around the attention partial kernel
+    # (recorded on the stream it runs on), nothing else.
+    every = max(1, args.event_every)
+    sampled = [i for i in range(steps) if i % every == 0] if args.events == "partial" else []
+    part_ev = {i: fresh_events(2) for i in sampled}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        t = warmup + i
+        ev = [None, part_ev[i][0], part_ev[i][1], None, None, None] if i in part_ev else None
+        dec.step_native(q[t], kn[t], vn[t], phase_events=ev)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    nh_dev = dec.cache.n_hi.cpu()
+    status = int(dec.cache.status.item())
+    if status != 0 or not bool((nh_dev == n_hi).all()):
+        log(f"[bench] ERROR: device status {status}, n_hi {nh_dev[:4].tolist()} vs tracked {n_hi}")
+        sys.exit(1)
+
+    # Diagnostics, untimed: an event at every phase boundary (each event adds
+    # a little time of its own to the phase it closes).
+    phases = ["append", "attn_partial", "attn_finalize", "importance", "select"]
+    ph_ev = [fresh_events(6) for _ in range(args.phase_steps)]
+    torch.cuda.synchronize()
+    for i in range(args.phase_steps):
+        t = warmup + steps + i
+        dec.step_native(q[t], kn[t], vn[t], phase_events=ph_ev[i])
+    torch.cuda.synchronize()
+    mean = lambda xs: sum(xs) / len(xs) if xs else float("nan")
+    dur = {p: [ph_ev[i][j].elapsed_time(ph_ev[i][j + 1]) for i in range(args.phase_steps)]
+           for j, p in enumerate(phases)}
+
+    # Diagnostics, untimed: whole steps bracketed by events, warm, then cold
+    # (the last-level cache and L2 flushed by reading 1 GiB before each
+    # step, outside the bracket; a read leaves no dirty lines behind).
+    mall = None
+    if args.mall_steps > 0:
+        flush = torch.zeros(1 << 28, dtype=torch.float32, device=dev)
+        mb, ln, nh = [], dec.length, int(dec.cache.n_hi[0].item())
+        for _ in range(2 * args.mall_steps):
+            ln, n_attn, nh = track_counts(dec, nh, ln)
+            mb.append(dec.cache.packed_bytes(ln, n_attn))
+        res = {}
+        base = warmup + steps + args.phase_steps
+        for j, kind in enumerate(("warm", "cold")):
+            evs = [fresh_events(2) for _ in range(args.mall_steps)]
+            torch.cuda.synchronize()
+            for i in range(args.mall_steps):
+                t = base + j * args.mall_steps + i
+                if kind == "cold":
+                    flush.sum()  # reads only: no dirty lines left to write back
+                evs[i][0].record()
+                dec.step_native(q[t], kn[t], vn[t])
+                evs[i][1].record()
+            torch.cuda.synchronize()
+            us = sorted(e[0].elapsed_time(e[1]) * 1e3 for e in evs)
+            nb = mb[j * args.mall_steps:(j + 1) * args.mall_steps]
+            res[kind] = {"step_us_median": round(us[len(us) // 2], 2), "step_us_mean": round(sum(us) / len(us), 2),
+                         "effective_GBps_median": round(sum(nb) / len(nb) / (us[len(us) // 2] * 1e-6) / 1e9, 1)}
+        del flush
+        mall = {**res, "steps_each": args.mall_steps, "flush": "1 GiB fp32 read (sum) before each cold step",
+                "note": "each step bracketed by two events on the stream (adds about empty_event_bracket_us)"}
+        log(f"[bench] {wl.name} whole step (event-bracketed): warm median {res['warm']['step_us_median']} us, "
+            f"cold median {res['cold']['step_us_median']} us")
+
+    total_bytes = sum(step_bytes)
+    value = total_bytes / elapsed / 1e9
+    ms = elapsed / steps * 1e3
+    mean_bytes = total_bytes / steps
+    roofline = None
+    if part_ev:
+        part_ms = [part_ev[i][0].elapsed_time(part_ev[i][1]) for i in sampled]
+        # per-launch algorithmic bytes / per-launch duration over the sampled
+        # launches (each counts with its own step's bytes)
+        achieved = sum(step_bytes[i] for i in sampled) / (sum(part_ms) * 1e-3) / 1e9
+        # An empty event bracket (the kernel-free "importance" phase of the
+        # fused step, measured in the diagnostic pass) shows the time the two
+        # events add to a bracketed launch.
+        overhead_ms = mean(dur["importance"]) if args.fused else float("nan")
+        tr = measured_traffic(wl.name) if not overridden else None
+        roofline = {"kernel": "attn_partial_kernel", "bound": "hbm", "achieved": round(achieved, 2),
+                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                    "traffic": tr["read_bytes"] + tr["write_bytes"] if tr else None,
+                    "traffic_unit": "HBM bytes per launch (read + write, rocprofv3 FETCH_SIZE/WRITE_SIZE, "
+                                    "copy-calibrated)",
+                    "mean_launch_us": round(mean(part_ms) * 1e3, 2),
+                    "launches_timed": len(part_ms), "launch_timing": f"HIP events on every {every}-th timed step",
+                    "empty_event_bracket_us": round(overhead_ms * 1e3, 2) if overhead_ms == overhead_ms else None,
+                    "algorithmic_bytes_per_launch": int(mean_bytes)}
+        if tr:
+            roofline["traffic_read_bytes"] = tr["read_bytes"]
+            roofline["traffic_write_bytes"] = tr["write_bytes"]
+    log(f"[bench] {wl.name}: {steps} steps in {elapsed * 1e3:.2f} ms: {ms * 1e3:.1f} us/step, "
+        f"{value:.1f} GB/s effective ({100 * value / HBM_PEAK_GBPS:.1f} % of peak)")
+    if roofline:
+        log(f"[bench] {wl.name} attn_partial: {roofline['mean_launch_us']} us/launch, {roofline['achieved']} GB/s")
+    log(f"[bench] {wl.name} phase means (us, diagnostic pass): " +
+        ", ".join(f"{p} {mean(dur[p]) * 1e3:.1f}" for p in phases))
+    del dec
+    torch.cuda.empty_cache()
+
+    cpu = None
+    if cpu_seconds > 0:
+        cpu = cpu_baseline(wl, (q, kn, vn), cpu_seconds)
+        log(f"[bench] {wl.name} cpu oracle: {cpu['value']} GB/s ({cpu['sample']}); one thread "
+            f"{cpu['single_thread']['value']} GB/s ({cpu['single_thread']['sample']})")
+    del q, kn, vn, steps_inputs
+    torch.cuda.empty_cache()
+    return {
+        "value": round(value, 2),
+        "ms_per_step": round(ms, 5),
+        "config": {"workload": wl.name, "batch": wl.batch, "q_heads": wl.q_heads, "kv_heads": wl.kv_heads,
+                   "head_dim": wl.head_dim, "context": wl.context, "hi_bits": wl.hi_bits, "lo_bits": wl.lo_bits,
+                   "group": wl.group, "ratio": f"{wl.ratio_num}/{wl.ratio_den}", "window": wl.window,
+                   "balanced": wl.balanced, "importance_fused": bool(args.fused),
+                   "parallelism": "single GPU"},
+        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
+        "steps_per_s": round(1e3 / ms, 1),
+        "packed_bytes_per_step": int(mean_bytes),
+        "phase_us": {p: round(mean(dur[p]) * 1e3, 2) for p in phases},
+        "roofline": roofline,
+        "mall": mall,
+        "cpu_baseline": cpu,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="long_context")
+    ap.add_argument("--secondary", default="llama2_13b",
+                    help="a second workload timed in the same run and reported under `secondary` ('' for none); "
+                         "it runs min(--steps, its own step count) timed steps")
     ap.add_argument("--fused", type=int, default=1, help="fuse the importance update into attention (default 1)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="time budget of the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="time budget of the CPU oracle baseline (all threads; one thread gets half)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--override", action="append", default=[], metavar="FIELD=VALUE",
                     help="change a workload field, e.g. ratio_num=0 (experiments; reported in config)")
@@ -243,184 +439,42 @@ def main():
               "this build measures one GPU's share and has no multi-GPU path.", file=sys.stderr)
         sys.exit(2)
 
-    import torch
-
-    from paper_2402_18096_amd import mikv, workloads
+    from paper_2402_18096_amd import workloads
 
     if args.copy_probe:
         return copy_probe(args.copy_probe)
     if args.prefill_importance:
         return prefill_importance_probe(args.workload, max(1, args.steps if args.steps < 256 else 3))
-    wl = workloads.WORKLOADS[args.workload]
-    for ov in args.override:
-        key, val = ov.split("=", 1)
-        cur = getattr(wl, key)
-        wl = wl.with_(**{key: type(cur)(val) if not isinstance(cur, bool) else val in ("1", "true", "True")})
-    dev = torch.device("cuda:0")
-    n_total = args.warmup + args.steps + args.phase_steps + 2 * args.mall_steps
-    t_setup = time.perf_counter()
-    dec = mikv.MikvDecoder(wl, max_len=wl.context + n_total, device=dev, fused=bool(args.fused))
-    k, v = workloads.prefill_kv(wl, dev)
-    sc = workloads.initial_scores(wl, dev)
-    qp = workloads.prefill_queries(wl, dev) if wl.balanced else None
-    steps_inputs = workloads.decode_inputs(wl, n_total, dev)
-    q, kn, vn = steps_inputs
-    dec.prefill(k, v, sc, qp)
-    del k, v, qp
-    torch.cuda.synchronize()
-    log(f"[bench] {wl.name}: prefill of {wl.context} tokens x {wl.n_heads} heads done "
-        f"({time.perf_counter() - t_setup:.1f} s); warmup {args.warmup}, timed {args.steps}")
-
-    for t in range(args.warmup):
-        dec.step_native(q[t], kn[t], vn[t])
-    torch.cuda.synchronize()
-
-    n_hi = int(dec.cache.n_hi[0].item())
-    length = dec.length
-    step_bytes = []
-    for _ in range(args.steps):
-        length, n_attn, n_hi = track_counts(dec, n_hi, length)
-        step_bytes.append(dec.cache.packed_bytes(length, n_attn))
-
-    def fresh_events(n):
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-        for e in evs:
-            e.record()
-        return evs
-
-    # Timed steps: two events per step around the attention partial kernel
-    # (recorded on the stream it runs on), nothing else.
-    every = max(1, args.event_every)
-    sampled = [i for i in range(args.steps) if i % every == 0] if args.events == "partial" else []
-    part_ev = {i: fresh_events(2) for i in sampled}
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        t = args.warmup + i
-        ev = [None, part_ev[i][0], part_ev[i][1], None, None, None] if i in part_ev else None
-        dec.step_native(q[t], kn[t], vn[t], phase_events=ev)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-
-    nh_dev = dec.cache.n_hi.cpu()
-    status = int(dec.cache.status.item())
-    if status != 0 or not bool((nh_dev == n_hi).all()):
-        log(f"[bench] ERROR: device status {status}, n_hi {nh_dev[:4].tolist()} vs tracked {n_hi}")
-        sys.exit(1)
-
-    # Diagnostics, untimed: an event at every phase boundary (each event adds
-    # a little time of its own to the phase it closes).
-    phases = ["append", "attn_partial", "attn_finalize", "importance", "select"]
-    ph_ev = [fresh_events(6) for _ in range(args.phase_steps)]
-    torch.cuda.synchronize()
-    for i in range(args.phase_steps):
-        t = args.warmup + args.steps + i
-        dec.step_native(q[t], kn[t], vn[t], phase_events=ph_ev[i])
-    torch.cuda.synchronize()
-    mean = lambda xs: sum(xs) / len(xs) if xs else float("nan")
-    dur = {p: [ph_ev[i][j].elapsed_time(ph_ev[i][j + 1]) for i in range(args.phase_steps)]
-           for j, p in enumerate(phases)}
-
-    # Diagnostics, untimed: whole steps bracketed by events, warm, then cold
-    # (the last-level cache and L2 flushed by reading 1 GiB before each
-    # step, outside the bracket; a read leaves no dirty lines behind).
-    mall = None
-    if args.mall_steps > 0:
-        flush = torch.zeros(1 << 28, dtype=torch.float32, device=dev)
-        mb, ln, nh = [], dec.length, int(dec.cache.n_hi[0].item())
-        for _ in range(2 * args.mall_steps):
-            ln, n_attn, nh = track_counts(dec, nh, ln)
-            mb.append(dec.cache.packed_bytes(ln, n_attn))
-        res = {}
-        base = args.warmup + args.steps + args.phase_steps
-        for j, kind in enumerate(("warm", "cold")):
-            evs = [fresh_events(2) for _ in range(args.mall_steps)]
-            torch.cuda.synchronize()
-            for i in range(args.mall_steps):
-                t = base + j * args.mall_steps + i
-                if kind == "cold":
-                    flush.sum()  # reads only: no dirty lines left to write back
-                evs[i][0].record()
-                dec.step_native(q[t], kn[t], vn[t])
-                evs[i][1].record()
-            torch.cuda.synchronize()
-            us = sorted(e[0].elapsed_time(e[1]) * 1e3 for e in evs)
-            nb = mb[j * args.mall_steps:(j + 1) * args.mall_steps]
-            res[kind] = {"step_us_median": round(us[len(us) // 2], 2), "step_us_mean": round(sum(us) / len(us), 2),
-                         "effective_GBps_median": round(sum(nb) / len(nb) / (us[len(us) // 2] * 1e-6) / 1e9, 1)}
-        del flush
-        mall = {**res, "steps_each": args.mall_steps, "flush": "1 GiB fp32 read (sum) before each cold step",
-                "note": "each step bracketed by two events on the stream (adds about empty_event_bracket_us)"}
-        log(f"[bench] whole step (event-bracketed): warm median {res['warm']['step_us_median']} us, "
-            f"cold median {res['cold']['step_us_median']} us")
-
-    total_bytes = sum(step_bytes)
-    value = total_bytes / elapsed / 1e9
-    ms = elapsed / args.steps * 1e3
-    mean_bytes = total_bytes / args.steps
-    roofline = None
-    if part_ev:
-        part_ms = [part_ev[i][0].elapsed_time(part_ev[i][1]) for i in sampled]
-        # per-launch algorithmic bytes / per-launch duration over the sampled
-        # launches (each counts with its own step's bytes)
-        achieved = sum(step_bytes[i] for i in sampled) / (sum(part_ms) * 1e-3) / 1e9
-        # An empty event bracket (the kernel-free "importance" phase of the
-        # fused step, measured in the diagnostic pass) shows the time the two
-        # events add to a bracketed launch.
-        overhead_ms = mean(dur["importance"]) if args.fused else float("nan")
-        tr = measured_traffic(wl.name) if not args.override else None
-        roofline = {"kernel": "attn_partial_kernel", "bound": "hbm", "achieved": round(achieved, 2),
-                    "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                    "traffic": tr["read_bytes"] + tr["write_bytes"] if tr else None,
-                    "traffic_unit": "HBM bytes per launch (read + write, rocprofv3 FETCH_SIZE/WRITE_SIZE, "
-                                    "copy-calibrated)",
-                    "mean_launch_us": round(mean(part_ms) * 1e3, 2),
-                    "launches_timed": len(part_ms), "launch_timing": f"HIP events on every {every}-th timed step",
-                    "empty_event_bracket_us": round(overhead_ms * 1e3, 2) if overhead_ms == overhead_ms else None,
-                    "algorithmic_bytes_per_launch": int(mean_bytes)}
-        if tr:
-            roofline["traffic_read_bytes"] = tr["read_bytes"]
-            roofline["traffic_write_bytes"] = tr["write_bytes"]
-    log(f"[bench] {args.steps} steps in {elapsed * 1e3:.2f} ms: {ms * 1e3:.1f} us/step, "
-        f"{value:.1f} GB/s effective ({100 * value / HBM_PEAK_GBPS:.1f} % of peak)")
-    if roofline:
-        log(f"[bench] attn_partial: {roofline['mean_launch_us']} us/launch, {roofline['achieved']} GB/s")
-    log("[bench] phase means (us, diagnostic pass): " +
-        ", ".join(f"{p} {mean(dur[p]) * 1e3:.1f}" for p in phases))
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, steps_inputs, args.cpu_seconds)
-        log(f"[bench] cpu oracle: {cpu['value']} GB/s ({cpu['sample']})")
-
+    wl = apply_overrides(workloads.WORKLOADS[args.workload], args.override)
+    cpu_s = 0.0 if args.no_cpu_baseline else args.cpu_seconds
+    head = run_workload(wl, args, args.steps, args.warmup, cpu_s, bool(args.override))
+    secondary = None
+    if args.secondary and args.secondary != args.workload:
+        wl2 = apply_overrides(workloads.WORKLOADS[args.secondary], args.override)
+        secondary = run_workload(wl2, args, min(args.steps, wl2.steps), args.warmup, cpu_s * 2 / 3,
+                                 bool(args.override))
+        secondary["steps"] = min(args.steps, wl2.steps)
+        secondary["warmup"] = args.warmup
     rec = {
         "metric": "mixed-KV decode attention effective GB/s (% of HBM peak) + decode steps/s",
-        "value": round(value, 2),
+        "value": head["value"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms, 5),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": wl.name, "batch": wl.batch, "q_heads": wl.q_heads, "kv_heads": wl.kv_heads,
-                   "head_dim": wl.head_dim, "context": wl.context, "hi_bits": wl.hi_bits, "lo_bits": wl.lo_bits,
-                   "group": wl.group, "ratio": f"{wl.ratio_num}/{wl.ratio_den}", "window": wl.window,
-                   "balanced": wl.balanced, "importance_fused": bool(args.fused),
-                   "parallelism": "single GPU"},
-        "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
-        "steps_per_s": round(1e3 / ms, 1),
-        "packed_bytes_per_step": int(mean_bytes),
-        "phase_us": {p: round(mean(dur[p]) * 1e3, 2) for p in phases},
-        "roofline": roofline,
-        "mall": mall,
-        "cpu_baseline": cpu,
+        **{k: v for k, v in head.items() if k not in ("value", "ms_per_step")},
+        "secondary": secondary,
     }
     if args.override:
         rec["config"]["overrides"] = args.override
+        if secondary:
+            secondary["config"]["overrides"] = args.override
     print(json.dumps(rec), flush=True)
 
 

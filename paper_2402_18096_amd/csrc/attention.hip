@@ -45,8 +45,10 @@ namespace {
 
 constexpr int kBlock = 256;        // finalize / importance kernels
 constexpr int kWaves = 1;          // the partial kernel runs one wave per chunk
-// Chunk record per query head and chunk: max, sum, two pad words, value
-// sum[128] (kept 16-byte aligned for vector loads).
+// Chunk record per query head and chunk: max, sum, the pool's token count
+// as the partial phase saw it (int32 bits), a pad word, value sum[128]
+// (kept 16-byte aligned for vector loads).
+constexpr int kRecN = 2;
 constexpr int kRecO = 4;
 constexpr int kRec = kRecO + kHeadDim;
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -555,6 +557,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
     if (lane == 0) {
       rec[0] = m2[i];
       rec[1] = l[i];
+      rec[kRecN] = __builtin_bit_cast(float, n_pool);
     }
     if (tsub == 0) {
       float4 *r4 = reinterpret_cast<float4 *>(rec + kRecO + part * CPL);
@@ -998,6 +1001,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
     if (lane == 0) {
       rec[0] = m2q[i];
       rec[1] = lq[i];
+      rec[kRecN] = __builtin_bit_cast(float, n_pool);
     }
     if (a == i / 2) {
       const int r0 = 2 * (i % 2);
@@ -1174,9 +1178,10 @@ struct ProbTile {
   int n_pool;
 };
 
+// n_pool: the pool's token count (< 0: read the live counter).
 template <int G>
 __device__ inline ProbTile<G> prob_tile_load(const AttnArgs &A, int h, int qh0, bool is_hi, int tile, bool has_tile,
-                                             bool accumulate) {
+                                             bool accumulate, int n_pool = -1) {
   ProbTile<G> T;
   const int cap = is_hi ? A.cap_hi : A.cap_lo;
   const float *scores = is_hi ? A.scores_hi : A.scores_lo;
@@ -1189,7 +1194,7 @@ __device__ inline ProbTile<G> prob_tile_load(const AttnArgs &A, int h, int qh0, 
     for (int i = 0; i < G; ++i) T.sv[u][i] = ok ? scores[(int64_t)(qh0 + i) * cap + T.t[u]] : 0.0f;
     T.a[u] = ok && acc ? acc[(int64_t)h * A.cap_hi + T.t[u]] : 0.0f;
   }
-  T.n_pool = has_tile ? (is_hi ? hi_count(A, h) : A.n_lo[h]) : 0;
+  T.n_pool = !has_tile ? 0 : n_pool >= 0 ? n_pool : is_hi ? hi_count(A, h) : A.n_lo[h];
   return T;
 }
 
@@ -1339,12 +1344,19 @@ __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int
   }
   if (c > 1) {
     // kLoTiles retained-pool tiles per block, all loaded before the
-    // statistics: fewer, longer blocks (one round of blocks per step)
+    // statistics: fewer, longer blocks (one round of blocks per step).
+    // Block (h, 0) raises n_lo when it demotes, concurrently with this
+    // block, so the retained pool's size at attention time comes from the
+    // record of the head's first retained-pool chunk, written by the
+    // partial phase.
     constexpr int KT = lo_tiles_per_block(G);
     const int t0 = (c - 2) * KT;
+    const int n_lo_att = __builtin_bit_cast(
+        int, A.partials[((int64_t)qh0 * nc + A.nc_hi) * kRec + kRecN]);
     ProbTile<G> T[KT];
 #pragma unroll
-    for (int k = 0; k < KT; ++k) T[k] = prob_tile_load<G>(A, h, qh0, false, t0 + k, t0 + k < tiles_lo, false);
+    for (int k = 0; k < KT; ++k)
+      T[k] = prob_tile_load<G>(A, h, qh0, false, t0 + k, t0 + k < tiles_lo, false, n_lo_att);
     float M[G], inv[G];
     head_stats<G>(A, qh0, nc, M, inv);
 #pragma unroll

@@ -380,7 +380,10 @@ def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
 @pytest.mark.parametrize("fused", [False, True])
 def test_native_step_matches_call_sequence(name, fused):
     """mikv_decode_step (one native call) leaves exactly the state that the
-    four separate calls leave, and the same outputs."""
+    four separate calls leave, and the same outputs: the attention output and
+    both probability buffers compared slot for slot over their whole
+    capacity, so a slot that only one of them writes (e.g. a retained-pool
+    slot filled by this step's demotion) shows up."""
     _dev()
     wl = workloads.small_workload(name, **SMALL[name])
     steps = 5
@@ -388,12 +391,27 @@ def test_native_step_matches_call_sequence(name, fused):
     run.prefill()
     other = mikv.MikvDecoder(wl, max_len=wl.context + steps, device="cuda", fused=fused)
     other.prefill(run.k.cuda(), run.v.cuda(), run.sc.cuda(), run.qp.cuda() if run.qp is not None else None)
+    # stale contents that a stray write would overwrite
+    for d in (run.dec, other):
+        d.probs_hi.fill_(-1.0)
+        d.probs_lo.fill_(-1.0)
     for t in range(steps):
+        n_lo0 = other.cache.n_lo.clone()
         run.step(t)
         other.step_native(run.q[t].cuda(), run.kn[t].cuda(), run.vn[t].cuda())
         torch.cuda.synchronize()
         compare_state(other.cache, run.orc, tag=f"native step {t}")
         np.testing.assert_array_equal(other.out.cpu().numpy(), run.dec.out.cpu().numpy())
+        np.testing.assert_array_equal(other.probs_hi.cpu().numpy().view(np.uint32),
+                                      run.dec.probs_hi.cpu().numpy().view(np.uint32), err_msg=f"step {t}: probs_hi")
+        np.testing.assert_array_equal(other.probs_lo.cpu().numpy().view(np.uint32),
+                                      run.dec.probs_lo.cpu().numpy().view(np.uint32), err_msg=f"step {t}: probs_lo")
+        # the slots this step's demotions filled were not attended: untouched
+        n_lo1 = other.cache.n_lo.cpu().numpy()
+        pl = other.probs_lo.cpu().numpy().reshape(wl.n_heads, wl.group_size, -1)
+        for h, (a, b) in enumerate(zip(n_lo0.cpu().numpy(), n_lo1)):
+            assert (pl[h, :, a:b] == -1.0).all(), f"step {t} head {h}: retained slots {a}..{b} written"
+
 
 
 def test_fp16_pool_rounding_edge_cases():
