@@ -15,7 +15,8 @@
  *  - All pointers named in a mikv_cache and every array argument are DEVICE
  *    pointers unless stated otherwise.  The caller allocates everything; the
  *    library allocates no memory and keeps no state between calls apart from
- *    its loaded code objects.
+ *    its loaded code objects (which hold the device scratch array of
+ *    mikv_decode_step_noalloc).
  *  - Every call is asynchronous on `stream` (a hipStream_t; NULL = the null
  *    stream).  Results are valid once the stream has synchronised.  Calls on
  *    distinct buffers are thread safe; overlapping calls on one cache race.
@@ -320,6 +321,29 @@ int mikv_decode_step(const mikv_cache *c, int32_t length, const uint16_t *q, con
                      const uint16_t *v_new, const float *balance, float scale, float *out, float *probs_hi,
                      float *probs_lo, int32_t k_heavy, int32_t window, int32_t flags, void *workspace,
                      size_t workspace_bytes, void *const *phase_events, void *stream);
+
+/*
+ * mikv_decode_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops or
+ * harnesses that forbid hipMalloc): the step's workspace is a device array
+ * inside the library, MIKV_DECODE_STEP_NOALLOC_MAX_WORKSPACE bytes on each
+ * GPU the library runs on, held until the process ends.  The call allocates
+ * nothing (no hipMalloc, hipFree or allocating library routine); the caller
+ * still passes every input and output.  Arguments and results are those of
+ * mikv_decode_step, on the current device (`stream` must belong to it).
+ * Every call on one GPU shares that GPU's array: calls that may overlap on
+ * one GPU (other streams, other threads) race and must not be issued; calls
+ * on one stream are ordered and safe.  The array keeps the last call's
+ * contents; nothing in it needs clearing between calls.
+ * Errors: those of mikv_decode_step; CAPACITY when
+ * mikv_decode_step_workspace_size(c, length) exceeds the array; HIP when the
+ * array's address cannot be obtained.
+ */
+#define MIKV_DECODE_STEP_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)
+int mikv_decode_step_noalloc(const mikv_cache *c, int32_t length, const uint16_t *q, const uint16_t *k_new,
+                             const uint16_t *v_new, const float *balance, float scale, float *out, float *probs_hi,
+                             float *probs_lo, int32_t k_heavy, int32_t window, int32_t flags,
+                             void *const *phase_events, void *stream);
 
 #ifdef __cplusplus
 }

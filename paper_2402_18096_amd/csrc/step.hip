@@ -3,6 +3,7 @@
 // A single host call keeps the step from being bound by per-call host
 // overhead; optional events mark the phase boundaries for profiling.
 #include <algorithm>
+#include <mutex>
 
 #include "mikv_internal.h"
 
@@ -99,4 +100,65 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
   if (rc) return rc;
   mark(5);
   return MIKV_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The decode step without a caller workspace, for callers that cannot
+// allocate device memory.  Its workspace is a file-scope device array; each
+// GPU the library runs on holds its own copy until the process ends.  In
+// host code the array's name is not a device address: its address on the
+// current device comes from hipGetSymbolAddress, once per device, and only
+// that pointer is handed to kernels.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t kScratchBytes = MIKV_DECODE_STEP_NOALLOC_MAX_WORKSPACE;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of the scratch array on the current device.
+int scratch_on_current_device(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return set_error(MIKV_ERR_HIP, "mikv_decode_step_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return set_error(MIKV_ERR_UNSUPPORTED, "mikv_decode_step_noalloc: device %d beyond the %d supported", dev,
+                     kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return set_error(MIKV_ERR_HIP, "mikv_decode_step_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MIKV_OK;
+}
+
+}  // namespace
+
+extern "C" int mikv_decode_step_noalloc(const mikv_cache *c, int32_t length, const uint16_t *q,
+                                        const uint16_t *k_new, const uint16_t *v_new, const float *balance,
+                                        float scale, float *out, float *probs_hi, float *probs_lo, int32_t k_heavy,
+                                        int32_t window, int32_t flags, void *const *phase_events, void *stream) {
+  int rc = validate_cache(c);
+  if (rc) return rc;
+  if (length < 1 || length > c->max_len)
+    return set_error(length < 1 ? MIKV_ERR_INVALID_ARG : MIKV_ERR_CAPACITY,
+                     "mikv_decode_step_noalloc: length %d outside [1, max_len]", length);
+  const size_t need = mikv_decode_step_workspace_size(c, length);
+  if (need > kScratchBytes)
+    return set_error(MIKV_ERR_CAPACITY,
+                     "mikv_decode_step_noalloc: the step needs %zu bytes of workspace, more than the %zu of the "
+                     "library's scratch array (use mikv_decode_step with a workspace)",
+                     need, kScratchBytes);
+  void *ws = nullptr;
+  rc = scratch_on_current_device(&ws);
+  if (rc) return rc;
+  return mikv_decode_step(c, length, q, k_new, v_new, balance, scale, out, probs_hi, probs_lo, k_heavy, window, flags,
+                          ws, kScratchBytes, phase_events, stream);
 }

@@ -72,6 +72,10 @@ _SIGS["mikv_decode_step"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p, c_void_
                                        c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p, c_size_t, c_void_p,
                                        c_void_p])
 
+_SIGS["mikv_decode_step_noalloc"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_float,
+                                               c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p,
+                                               c_void_p])
+
 EXPORTS = tuple(_SIGS)
 
 
@@ -324,6 +328,23 @@ def mikv_decode_step(cache: MikvCache, length: int, q, k_new, v_new, out, k_heav
     _check(L.mikv_decode_step(cache.ref(), length, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(balance), scale,
                               _ptr(out), _ptr(probs_hi), _ptr(probs_lo), k_heavy, window, flags, _ptr(ws),
                               ws.numel(), ev, _stream()), "mikv_decode_step")
+
+
+def mikv_decode_step_noalloc(cache: MikvCache, length: int, q, k_new, v_new, out, k_heavy: int, window: int,
+                             probs_hi=None, probs_lo=None, balance=None, scale=None, flags=0, phase_events=None):
+    """mikv_decode_step with the library's own device scratch array as its
+    workspace: nothing is allocated, here or in the library."""
+    _require(q, torch.float16, (cache.batch, cache.q_heads, HEAD_DIM), "q")
+    _require(k_new, torch.float16, (cache.batch, cache.kv_heads, HEAD_DIM), "k_new")
+    _require(v_new, torch.float16, (cache.batch, cache.kv_heads, HEAD_DIM), "v_new")
+    _require(out, torch.float32, (cache.batch, cache.q_heads, HEAD_DIM), "out")
+    ev = None
+    if phase_events is not None:
+        ev = (c_void_p * 6)(*[e.cuda_event if e is not None else None for e in phase_events])
+    scale = 1.0 / math.sqrt(HEAD_DIM) if scale is None else scale
+    _check(lib().mikv_decode_step_noalloc(cache.ref(), length, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(balance),
+                                          scale, _ptr(out), _ptr(probs_hi), _ptr(probs_lo), k_heavy, window, flags,
+                                          ev, _stream()), "mikv_decode_step_noalloc")
 
 
 # -- the method's step sequence ---------------------------------------------------

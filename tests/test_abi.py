@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 18
+    assert len(names) == 19
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -121,3 +121,17 @@ def test_workspace_sizes_are_consistent():
     assert a >= 4 * 4 * 100   # at least the scores scratch of the importance pool
     assert L.mikv_select_workspace_size(ctypes.byref(c)) == 2 * 4 * 1 * 4 * 100
     assert L.mikv_balance_workspace_size(1, 4, 1000) > 0
+
+
+def test_noalloc_step_rejects_a_workspace_beyond_its_scratch_array():
+    """mikv_decode_step_noalloc refuses, on the host and before touching the
+    device, a step whose workspace exceeds the library's scratch array."""
+    c = _desc(batch=96, q_heads=40, kv_heads=40, hi_bits=8, cap_hi=1764, cap_lo=8504, max_len=8504)
+    c.hi_kp = c.hi_vp = 0x1000
+    L = mikv.lib()
+    assert L.mikv_decode_step_workspace_size(ctypes.byref(c), 8400) > (64 << 20)
+    p = ctypes.c_void_p(0x1000)
+    rc = L.mikv_decode_step_noalloc(ctypes.byref(c), 8400, p, p, p, None, 0.1, p, None, None, 10, 64,
+                                    mikv.ATTN_ACCUMULATE, None, None)
+    assert rc == 3
+    assert b"scratch" in L.mikv_last_error()
