@@ -271,12 +271,30 @@ int mikv_importance_update(const mikv_cache *c, int32_t length, const float *pro
  * (keys are already balanced; with lo_bits 0 it is dropped instead), its
  * map entry set to 0, and its importance slot is
  * refilled from the end of the pool.  Demotion is one way.
+ *   heavy_idx int32 [B, Hkv, k_heavy] or NULL (output): the positions of the
+ *             kept eligible tokens (the heavy hitters), most important
+ *             first by the same key (score descending, an exact score tie
+ *             to the larger position); entries past the number kept are -1.
+ *             Requires cap_hi <= 8192 (UNSUPPORTED otherwise).
  *   workspace at least mikv_select_workspace_size(c) bytes.
- * Errors: INVALID_ARG (k_heavy < 0, window < 0, length > max_len), CAPACITY.
+ * Errors: INVALID_ARG (k_heavy < 0, window < 0, length > max_len), CAPACITY,
+ * UNSUPPORTED (heavy list with cap_hi > 8192).
  */
 size_t mikv_select_workspace_size(const mikv_cache *c);
 int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window,
-                     void *workspace, size_t workspace_bytes, void *stream);
+                     int32_t *heavy_idx, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * High-precision budget of the re-rank (Section 3.1: a fixed ratio of the
+ * cache kept at high precision; Fig. 3 right): the number of tokens outside
+ * the recent window kept for their accumulated attention in a cache of
+ * `length` tokens,
+ *   k_heavy = max(0, floor(length * ratio_num / ratio_den) - (window_in_ratio ? window : 0)),
+ * in 64-bit integer arithmetic.  A host function (no device work); -1 for a
+ * negative length, ratio_num or window, or ratio_den < 1.
+ */
+int32_t mikv_heavy_budget(int32_t length, int32_t ratio_num, int32_t ratio_den, int32_t window,
+                          int32_t window_in_ratio);
 
 /*
  * First selection after prefill: every token outside the window is eligible.

@@ -19,11 +19,11 @@ properties that do not come from the oracle itself.
 from .attention import attention
 from .balance import balance_keys, balance_query, balancer
 from .cache import OracleCache
-from .policy import accumulate, heavy_budget, prefill_importance, select
+from .policy import accumulate, heavy_budget, heavy_list, prefill_importance, select
 from .quant import bits_per_element, dequantize, f16_bits, f16_value, pack, quantize, unpack
 
 __all__ = [
     "attention", "balance_keys", "balance_query", "balancer", "OracleCache", "accumulate",
-    "heavy_budget", "prefill_importance", "select", "bits_per_element", "dequantize", "f16_bits", "f16_value", "pack",
+    "heavy_budget", "heavy_list", "prefill_importance", "select", "bits_per_element", "dequantize", "f16_bits", "f16_value", "pack",
     "quantize", "unpack",
 ]

@@ -68,6 +68,17 @@ def select(acc, is_hi, length: int, k_heavy: int, window: int, initial: bool) ->
     return new_hi
 
 
+def heavy_list(acc, is_hi, length: int, window: int) -> np.ndarray:
+    """The heavy hitters after a selection, most important first: the
+    high-precision positions outside the window, ordered by score
+    descending, an exact score tie to the newer position (the selection's
+    own order).  Returns int64 positions."""
+    acc = np.asarray(acc, dtype=np.float32)[:length]
+    pos = np.arange(length)
+    idx = pos[np.asarray(is_hi, dtype=bool)[:length] & (pos < length - window)]
+    return idx[np.lexsort((-idx, -acc[idx]))]
+
+
 def prefill_importance(q16, k16, scale: float) -> np.ndarray:
     """H2O importance of the prompt tokens at the end of prefill.
 

@@ -37,6 +37,55 @@ __global__ __launch_bounds__(kSel) void select_prefill_kernel(const float *score
   }
 }
 
+// The sorted heavy-token list (Fig. 3 right: the tokens the re-rank kept
+// for their accumulated attention): per head, the importance-pool tokens
+// outside the window, most important first by the rank key (score
+// descending, an exact tie to the newer token).  One block per head sorts
+// the pool's keys in LDS with a bitonic network (window tokens and empty
+// slots get key 0, below every real key, so they sort last).
+constexpr int kHeavyMaxSlots = 8192;  // importance-pool slots a head may hold for the list (64 KiB of keys)
+
+__global__ __launch_bounds__(kSel) void heavy_list_kernel(const int32_t *n_hi, const int32_t *hi_pos,
+                                                          const float *hi_acc, int cap_hi, int P, int thr, int k_heavy,
+                                                          int32_t *heavy_idx) {
+  extern __shared__ uint64_t s_key[];  // [P], P a power of two >= cap_hi
+  const int h = blockIdx.x;
+  const int n = min(n_hi[h], cap_hi);
+  const int32_t *pos = hi_pos + (int64_t)h * cap_hi;
+  const float *acc = hi_acc + (int64_t)h * cap_hi;
+  for (int i = threadIdx.x; i < P; i += kSel) {
+    uint64_t k = 0;
+    if (i < n) {
+      const int p = pos[i];
+      if (p < thr) k = rank_key(acc[i], p);
+    }
+    s_key[i] = k;
+  }
+  __syncthreads();
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = threadIdx.x; i < P; i += kSel) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint64_t a = s_key[i], b = s_key[l];
+          // descending overall: runs with (i & k) == 0 descend, the others ascend
+          const bool swap = (i & k) == 0 ? a < b : a > b;
+          if (swap) {
+            s_key[i] = b;
+            s_key[l] = a;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  int32_t *out = heavy_idx + (int64_t)h * k_heavy;
+  for (int r = threadIdx.x; r < k_heavy; r += kSel) {
+    const uint64_t k = r < P ? s_key[r] : 0;
+    out[r] = k != 0 ? (int32_t)(uint32_t)(k & 0xffffffffu) : -1;
+  }
+}
+
 template <int HI, int LO>
 void launch_select(const SelArgs &A, int NH, hipStream_t st) {
   hipLaunchKernelGGL((select_kernel<HI, LO>), dim3(NH), dim3(kSel), 0, st, A);
@@ -84,9 +133,27 @@ int select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t wi
 
 }  // namespace mikv
 
-extern "C" int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window, void *ws,
-                                size_t ws_bytes, void *stream) {
-  return select_topk(c, length, k_heavy, window, ws, ws_bytes, false, (hipStream_t)stream);
+extern "C" int mikv_select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t window,
+                                int32_t *heavy_idx, void *ws, size_t ws_bytes, void *stream) {
+  if (heavy_idx && c && c->cap_hi > kHeavyMaxSlots)
+    return set_error(MIKV_ERR_UNSUPPORTED, "mikv_select_topk: the heavy list needs cap_hi <= %d (got %d)",
+                     kHeavyMaxSlots, c->cap_hi);
+  int rc = select_topk(c, length, k_heavy, window, ws, ws_bytes, false, (hipStream_t)stream);
+  if (rc || !heavy_idx || k_heavy == 0) return rc;
+  int P = 1;
+  while (P < c->cap_hi) P <<= 1;
+  const int thr = std::max(0, length - window);
+  hipLaunchKernelGGL(heavy_list_kernel, dim3(n_heads_of(c)), dim3(kSel), (size_t)P * sizeof(uint64_t),
+                     (hipStream_t)stream, c->n_hi, c->hi_pos, c->hi_acc, c->cap_hi, P, thr, k_heavy, heavy_idx);
+  return check_launch("mikv_select_topk (heavy list)");
+}
+
+extern "C" int32_t mikv_heavy_budget(int32_t length, int32_t ratio_num, int32_t ratio_den, int32_t window,
+                                     int32_t window_in_ratio) {
+  if (length < 0 || ratio_num < 0 || ratio_den < 1 || window < 0) return -1;
+  int64_t k = (int64_t)ratio_num * length / ratio_den;
+  if (window_in_ratio) k -= window;
+  return (int32_t)std::max<int64_t>(0, k);
 }
 
 extern "C" int mikv_select_prefill(const float *scores, int32_t n_heads, int32_t length, int32_t k_heavy,

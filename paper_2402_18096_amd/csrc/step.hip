@@ -96,7 +96,7 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
   rc = mikv_importance_update(c, length, probs_hi, stream);
   if (rc) return rc;
   mark(4);
-  rc = mikv_select_topk(c, length, k_heavy, window, ws + attn_ws, workspace_bytes - attn_ws, stream);
+  rc = mikv_select_topk(c, length, k_heavy, window, nullptr, ws + attn_ws, workspace_bytes - attn_ws, stream);
   if (rc) return rc;
   mark(5);
   return MIKV_OK;

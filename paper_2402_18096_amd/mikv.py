@@ -60,7 +60,8 @@ _SIGS = {
     "mikv_decode_workspace_size": (c_size_t, [_PC, c_int32]),
     "mikv_importance_update": (c_int32, [_PC, c_int32, c_void_p, c_void_p]),
     "mikv_select_workspace_size": (c_size_t, [_PC]),
-    "mikv_select_topk": (c_int32, [_PC, c_int32, c_int32, c_int32, c_void_p, c_size_t, c_void_p]),
+    "mikv_select_topk": (c_int32, [_PC, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_size_t, c_void_p]),
+    "mikv_heavy_budget": (c_int32, [c_int32, c_int32, c_int32, c_int32, c_int32]),
     "mikv_select_prefill": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p]),
 }
 for _n in ("mikv_decode_attention", "mikv_decode_attention_partial", "mikv_decode_attention_finalize"):
@@ -293,12 +294,14 @@ def mikv_importance_update(cache: MikvCache, length: int, probs_hi: torch.Tensor
 
 
 def mikv_select_topk(cache: MikvCache, length: int, k_heavy: int, window: int,
-                     workspace: Optional[torch.Tensor] = None):
+                     workspace: Optional[torch.Tensor] = None, heavy_idx: Optional[torch.Tensor] = None):
     L = lib()
+    if heavy_idx is not None:
+        _require(heavy_idx, torch.int32, (cache.batch, cache.kv_heads, k_heavy), "heavy_idx")
     ws = workspace if workspace is not None else _workspace(L.mikv_select_workspace_size(cache.ref()),
                                                             cache.device)
-    _check(L.mikv_select_topk(cache.ref(), length, k_heavy, window, _ptr(ws), ws.numel(), _stream()),
-           "mikv_select_topk")
+    _check(L.mikv_select_topk(cache.ref(), length, k_heavy, window, _ptr(heavy_idx), _ptr(ws), ws.numel(),
+                              _stream()), "mikv_select_topk")
 
 
 def mikv_select_prefill(scores: torch.Tensor, k_heavy: int, window: int, hi_mask: torch.Tensor):
@@ -350,12 +353,13 @@ def mikv_decode_step_noalloc(cache: MikvCache, length: int, q, k_new, v_new, out
 # -- the method's step sequence ---------------------------------------------------
 
 def heavy_budget(length: int, ratio_num: int, ratio_den: int, window: int, window_in_ratio: bool) -> int:
-    """High-precision tokens outside the window for a cache of `length`:
-    floor(ratio * length), less the window when it counts towards the ratio."""
-    k = (ratio_num * length) // ratio_den
-    if window_in_ratio:
-        k -= window
-    return max(0, k)
+    """High-precision tokens outside the window for a cache of `length`
+    (mikv_heavy_budget: floor(ratio * length), less the window when it counts
+    towards the ratio)."""
+    k = lib().mikv_heavy_budget(length, ratio_num, ratio_den, window, int(bool(window_in_ratio)))
+    if k < 0:
+        raise MikvError(f"mikv_heavy_budget: invalid arguments ({length}, {ratio_num}/{ratio_den}, {window})")
+    return int(k)
 
 
 class MikvDecoder:
@@ -378,6 +382,7 @@ class MikvDecoder:
         c = self.cache
         self.length = 0
         self.balance = None
+        self.heavy_idx = None
         B, Hq = wl.batch, wl.q_heads
         self.out = torch.zeros(B, Hq, HEAD_DIM, dtype=torch.float32, device=self.device)
         self.probs_hi = torch.zeros(B, Hq, c.cap_hi, dtype=torch.float32, device=self.device)
@@ -414,10 +419,12 @@ class MikvDecoder:
         self.length = T
 
     def step(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, emit_lo: bool = True,
-             after_attention=None):
+             after_attention=None, emit_heavy: bool = False):
         """One decode step; q fp16 [B, Hq, D], k_new/v_new fp16 [B, Hkv, D].
         ``after_attention`` (optional) is called between attention and the
-        importance update, e.g. to snapshot the slot-ordered probabilities."""
+        importance update, e.g. to snapshot the slot-ordered probabilities;
+        with ``emit_heavy`` the re-rank also writes the sorted heavy-token
+        list to ``self.heavy_idx`` [B, Hkv, k_heavy]."""
         c = self.cache
         mikv_quantize_kv(c, k_new.unsqueeze(2), v_new.unsqueeze(2), self.length, self.balance)
         self.length += 1
@@ -429,7 +436,12 @@ class MikvDecoder:
             after_attention()
         if not self.fused:
             mikv_importance_update(c, L, self.probs_hi)
-        mikv_select_topk(c, L, self.k_heavy(L), self.wl.window, self.sel_ws)
+        kh = self.k_heavy(L)
+        heavy = None
+        if emit_heavy:
+            heavy = torch.empty(c.batch, c.kv_heads, kh, dtype=torch.int32, device=self.device)
+        mikv_select_topk(c, L, kh, self.wl.window, self.sel_ws, heavy)
+        self.heavy_idx = heavy
         return self.out
 
     def step_native(self, q: torch.Tensor, k_new: torch.Tensor, v_new: torch.Tensor, emit_lo: bool = True,

@@ -165,7 +165,8 @@ class Lockstep:
             snap["p_lo"] = self.dec.probs_lo.clone()
             snap["out"] = self.dec.out.cpu().numpy()
 
-        self.dec.step(self.q[t].cuda(), self.kn[t].cuda(), self.vn[t].cuda(), after_attention=after_attention)
+        self.dec.step(self.q[t].cuda(), self.kn[t].cuda(), self.vn[t].cuda(), after_attention=after_attention,
+                      emit_heavy=self.dec.cache.cap_hi <= 8192)
         torch.cuda.synchronize()
         L = self.dec.length
         self.orc.append(np16(self.kn[t]).reshape(NH, 128), np16(self.vn[t]).reshape(NH, 128), self.bal)
@@ -182,6 +183,14 @@ class Lockstep:
         self.orc.select(kh, wl.window)
         if check_state:
             compare_state(self.dec.cache, self.orc, tag=f"step {t}")
+        if self.dec.heavy_idx is not None:
+            # the sorted heavy-token list of the re-rank, bit for bit
+            got = self.dec.heavy_idx.cpu().numpy().reshape(NH, kh)
+            for h in range(NH):
+                want = np.full(kh, -1, np.int64)
+                hl = oracle.heavy_list(self.orc.acc[h], self.orc.is_hi[h], L, wl.window)[:kh]
+                want[:len(hl)] = hl
+                np.testing.assert_array_equal(got[h], want, err_msg=f"step {t} head {h}: heavy list")
         err_o = float(np.max(np.abs(o_gpu - o_ref)))
         err_p = float(np.max(np.abs(p_gpu - p_ref) / np.maximum(np.abs(p_ref), 1e-30)))
         return err_o, err_p

@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 19
+    assert len(names) == 20
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -93,7 +93,10 @@ def test_null_pointers_and_capacity():
     assert L.mikv_quantize_rows(None, 4, 128, None, 1, 2, 32, None, None, None) == 1
     assert L.mikv_quantize_rows(ctypes.c_void_p(1), 4, 128, None, 1, 5, 32, ctypes.c_void_p(1),
                                 ctypes.c_void_p(1), None) == 2
-    assert L.mikv_select_topk(ctypes.byref(_desc()), 4, -1, 0, ctypes.c_void_p(1), 1 << 20, None) == 1
+    assert L.mikv_select_topk(ctypes.byref(_desc()), 4, -1, 0, None, ctypes.c_void_p(1), 1 << 20, None) == 1
+    # the heavy list is limited to 8192 importance-pool slots per head
+    assert L.mikv_select_topk(ctypes.byref(_desc(cap_hi=9000, max_len=9000)), 4, 1, 0, ctypes.c_void_p(1),
+                              ctypes.c_void_p(1), 1 << 30, None) == 2
     assert L.mikv_select_prefill(None, 1, 4, 1, 1, None, None) == 1
     assert L.mikv_balance_channels(ctypes.c_void_p(1), ctypes.c_void_p(1), 1, 4, 4, 8, 64, ctypes.c_void_p(1),
                                    ctypes.c_void_p(1), 1 << 20, None) == 2
@@ -135,3 +138,16 @@ def test_noalloc_step_rejects_a_workspace_beyond_its_scratch_array():
                                     mikv.ATTN_ACCUMULATE, None, None)
     assert rc == 3
     assert b"scratch" in L.mikv_last_error()
+
+
+def test_heavy_budget():
+    """The re-rank's budget: floor(ratio * length), less the window when it
+    counts towards the ratio, never negative; invalid arguments give -1."""
+    L = mikv.lib()
+    assert L.mikv_heavy_budget(513, 1, 5, 32, 0) == 102          # top 20 % plus the last 32
+    assert L.mikv_heavy_budget(4097, 1, 4, 64, 1) == 960
+    assert L.mikv_heavy_budget(32769, 1, 10, 128, 1) == 3148
+    assert L.mikv_heavy_budget(100, 1, 10, 128, 1) == 0
+    assert L.mikv_heavy_budget(2 ** 31 - 1, 3, 4, 0, 0) == (2 ** 31 - 1) * 3 // 4   # no 32-bit overflow
+    assert L.mikv_heavy_budget(10, 1, 0, 0, 0) == -1
+    assert L.mikv_heavy_budget(-1, 1, 2, 0, 0) == -1

@@ -166,6 +166,30 @@ def test_select_brute_force_small():
         assert set(np.nonzero(got)[0].tolist()) == expect, (L, W, k, acc, is_hi, initial)
 
 
+def test_heavy_list_worked_example_and_brute_force():
+    """The heavy list is the kept non-window set in (score desc, position
+    desc) order: the worked example gives [0, 2] (position 4 is the window);
+    on random tiny inputs with many ties it is the kept set sorted by
+    Python's tuple order, and every adjacent pair is strictly decreasing in
+    (score, position)."""
+    acc = np.array([0.5, 0.25, 0.25, 0.125, 0.9], np.float32)
+    hi = oracle.select(acc, None, 5, 2, 1, initial=True)
+    assert oracle.heavy_list(acc, hi, 5, 1).tolist() == [0, 2]
+    acc2 = np.array([0.25, 0.25, 0.5, 0.25, 0.0], np.float32)
+    assert oracle.heavy_list(acc2, np.ones(5, bool), 5, 1).tolist() == [2, 3, 1, 0]
+    rng = np.random.default_rng(9)
+    for _ in range(100):
+        L = int(rng.integers(1, 30))
+        W = int(rng.integers(0, 5))
+        a = (rng.integers(0, 5, L) / 4).astype(np.float32)
+        m = rng.random(L) < 0.6
+        got = oracle.heavy_list(a, m, L, W).tolist()
+        want = [j for _, j in sorted(((float(a[j]), j) for j in range(L) if m[j] and j < L - W), reverse=True)]
+        assert got == want
+        for x, y in zip(got, got[1:]):
+            assert (a[x], x) > (a[y], y)
+
+
 def test_select_invariants():
     rng = np.random.default_rng(8)
     L, W, k = 1000, 64, 136
