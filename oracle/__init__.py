@@ -20,10 +20,11 @@ from .attention import attention
 from .balance import balance_keys, balance_query, balancer
 from .cache import OracleCache
 from .policy import accumulate, heavy_budget, heavy_list, prefill_importance, select
-from .quant import bits_per_element, dequantize, f16_bits, f16_value, pack, quantize, unpack
+from .quant import (bits_per_element, dequantize, encode, f16_bits, f16_value, pack, quantize, quantize_channels,
+                    unpack)
 
 __all__ = [
     "attention", "balance_keys", "balance_query", "balancer", "OracleCache", "accumulate",
     "heavy_budget", "heavy_list", "prefill_importance", "select", "bits_per_element", "dequantize", "f16_bits", "f16_value", "pack",
-    "quantize", "unpack",
+    "quantize", "unpack", "encode", "quantize_channels",
 ]

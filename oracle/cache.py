@@ -23,6 +23,24 @@ token outside the window is eligible, scored by the supplied initial scores.
 retained cache of 0 bits, Section 4 / Table 1): a token outside the
 importance cache is dropped, and attention runs over the importance cache
 alone (its probabilities are 0 at evicted positions).
+
+``key_block = 64`` is the per-channel key quantization of Appendix C: the
+retained cache's keys are quantized per channel over blocks of 64
+consecutive positions (Eq. 1 with token and channel exchanged), values stay
+per token.  Readings where the appendix is silent (it only simulates the
+scheme, quantizing keys as they are, without reordering):
+  * a block's parameters come from all 64 of its keys, whatever their
+    precision, taken from the fp16 keys as given (prefill) or as the
+    importance cache holds them (a block completed during decoding);
+  * a block is quantized once, when its last position arrives; with a window
+    of at least 64 positions all keys of a block that is not complete are in
+    the importance cache, so a retained key always has its block's
+    parameters;
+  * a token's key codes are those of its block at the time it is demoted
+    (the same codes as quantizing the whole block at once: a code depends
+    only on the key and the block's parameters);
+  * the importance cache is fp16, and no channel balancer is applied (the
+    per-channel quantizer takes the balancer's place in Table 6).
 """
 from __future__ import annotations
 
@@ -31,7 +49,7 @@ import numpy as np
 from .attention import attention
 from .balance import balance_keys
 from .policy import accumulate, select
-from .quant import dequantize, f16_bits, f16_value, quantize
+from .quant import dequantize, encode, f16_bits, f16_value, quantize, quantize_channels
 
 
 class OracleCache:
@@ -39,10 +57,18 @@ class OracleCache:
     head) pairs, each serving ``group_size`` query heads."""
 
     def __init__(self, n_heads: int, group_size: int, max_len: int, hi_bits: int, lo_bits: int,
-                 group: int, head_dim: int = 128):
+                 group: int, head_dim: int = 128, key_block: int = 0):
         assert hi_bits in (16, 8, 4) and lo_bits in (0, 2, 3, 4, 8)
+        assert key_block in (0, 64) and (key_block == 0 or (hi_bits == 16 and lo_bits in (2, 3, 4)))
         self.n_heads, self.G, self.max_len = n_heads, group_size, max_len
         self.hi_bits, self.lo_bits, self.group, self.d = hi_bits, lo_bits, group, head_dim
+        self.key_block = key_block
+        if key_block:
+            # per-channel key parameters of each block of key_block positions
+            nb = max_len // key_block
+            self.kb_a = np.zeros((n_heads, nb, head_dim), np.uint16)
+            self.kb_b = np.zeros((n_heads, nb, head_dim), np.uint16)
+            self.kb_done = np.zeros((n_heads, nb), bool)
         ng = head_dim // group
         shape, pshape = (n_heads, max_len, head_dim), (n_heads, max_len, ng)
         self.is_hi = np.zeros((n_heads, max_len), dtype=bool)
@@ -73,8 +99,18 @@ class OracleCache:
         n = self.lo_bits
         if n == 0:  # evicted: nothing is kept
             return
-        self.lk[h, pos], self.lk_a[h, pos], self.lk_b[h, pos] = quantize(kx, n, self.group)
+        if self.key_block:
+            blk = np.asarray(pos) // self.key_block
+            assert self.kb_done[h, blk].all(), "retained key of a block that is not complete"
+            self.lk[h, pos] = encode(kx, self.kb_a[h, blk], self.kb_b[h, blk], n)
+        else:
+            self.lk[h, pos], self.lk_a[h, pos], self.lk_b[h, pos] = quantize(kx, n, self.group)
         self.lv[h, pos], self.lv_a[h, pos], self.lv_b[h, pos] = quantize(vx, n, self.group)
+
+    def _close_block(self, h, blk, keys):
+        """Per-channel parameters of key block ``blk`` from its keys fp32 [64, D]."""
+        _, self.kb_a[h, blk], self.kb_b[h, blk] = quantize_channels(keys, self.lo_bits)
+        self.kb_done[h, blk] = True
 
     def _hi_values(self, h, pos):
         if self.hi_bits == 16:
@@ -85,8 +121,13 @@ class OracleCache:
 
     def _lo_values(self, h, pos):
         g = self.group
-        return (dequantize(self.lk[h, pos], self.lk_a[h, pos], self.lk_b[h, pos], g),
-                dequantize(self.lv[h, pos], self.lv_a[h, pos], self.lv_b[h, pos], g))
+        if self.key_block:
+            blk = np.asarray(pos) // self.key_block
+            # alpha * code + beta per channel with the block's parameters
+            k = f16_value(self.kb_a[h, blk]) * self.lk[h, pos].astype(np.float32) + f16_value(self.kb_b[h, blk])
+        else:
+            k = dequantize(self.lk[h, pos], self.lk_a[h, pos], self.lk_b[h, pos], g)
+        return k, dequantize(self.lv[h, pos], self.lv_a[h, pos], self.lv_b[h, pos], g)
 
     def values(self, h):
         """Decoded fp32 keys and values [L, D] of head ``h`` in position order."""
@@ -107,12 +148,17 @@ class OracleCache:
         """k16, v16 fp16 [H, T, D]; scores fp32 [H, T]; balance fp32 [H, D] or None."""
         H, T, _ = np.shape(k16)
         assert H == self.n_heads and T <= self.max_len
+        assert not self.key_block or (balance is None and window >= self.key_block)
         for h in range(H):
             hi = select(scores[h], None, T, k_heavy, window, initial=True)
             kx = balance_keys(k16[h], balance[h]) if balance is not None else \
                 np.asarray(k16[h], np.float16).astype(np.float32)
             vx = np.asarray(v16[h], np.float16).astype(np.float32)
             pos = np.arange(T)
+            if self.key_block:  # every complete block of the prompt, from its keys as given
+                kb = self.key_block
+                for blk in range(T // kb):
+                    self._close_block(h, blk, kx[blk * kb:(blk + 1) * kb])
             self._store_hi(h, pos[hi], kx[hi], vx[hi])
             self._store_lo(h, pos[~hi], kx[~hi], vx[~hi])
             self.is_hi[h, :T] = hi
@@ -130,6 +176,12 @@ class OracleCache:
             self._store_hi(h, pos, kx, vx)
             self.is_hi[h, pos] = True
             self.acc[h, pos] = 0.0
+            kb = self.key_block
+            if kb and (pos + 1) % kb == 0:  # the token completes a block: quantize it per channel
+                blk = pos // kb
+                span = np.arange(blk * kb, pos + 1)
+                assert self.is_hi[h, span].all(), "a block completes with keys outside the importance cache"
+                self._close_block(h, blk, f16_value(self.hk[h, span]))
         self.length = pos + 1
 
     def attend(self, q16, scale: float, balance=None):

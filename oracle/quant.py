@@ -62,6 +62,31 @@ def quantize(x, bits: int, group: int):
     return codes.reshape(*lead, d), alpha16, beta16
 
 
+def encode(x, alpha16, beta16, bits: int) -> np.ndarray:
+    """Eq. 1 codes of ``x`` (fp32, [..., D]) for given stored parameters
+    alpha16, beta16 (uint16 fp16 bits broadcastable to x): the encode step of
+    :func:`quantize` with the parameters supplied instead of derived."""
+    x = np.asarray(x, dtype=np.float32)
+    a = f16_value(alpha16)
+    b = f16_value(beta16)
+    top = np.float32(2 ** bits - 1)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        t = np.rint((x - b) / a)                    # round((x - beta) / alpha)
+    t = np.where(a == 0, np.float32(0), t)          # degenerate parameters
+    return np.clip(t, np.float32(0), top).astype(np.uint8)
+
+
+def quantize_channels(x_block, bits: int):
+    """Eq. 1 per channel over a block of tokens (the per-channel key
+    quantization of Appendix C): x_block fp32 [T, D] -> (codes uint8 [T, D],
+    alpha16 uint16 [D], beta16 uint16 [D]), i.e. the per-token quantizer with
+    the roles of token and channel exchanged (one group = one channel's T
+    values)."""
+    xt = np.asarray(x_block, dtype=np.float32).T             # [D, T]
+    codes, a16, b16 = quantize(xt, bits, xt.shape[-1])
+    return codes.T.copy(), a16[:, 0], b16[:, 0]
+
+
 def dequantize(codes, alpha16, beta16, group: int) -> np.ndarray:
     """Eq. 1 decode: alpha * code + beta in fp32 (the product is exact for an
     fp16 alpha and a code below 256, so this has a single rounding)."""
@@ -102,7 +127,8 @@ def unpack(packed, bits: int) -> np.ndarray:
 
 def bits_per_element(bits: int, group: int) -> float:
     """Storage cost of one quantized element: the code plus its share of the
-    fp16 scale and zero point of its group; fp16 storage costs 16 bits."""
+    fp16 scale and zero point of its group; fp16 storage costs 16 bits.  A
+    per-channel group of ``group`` tokens costs the same share."""
     if bits == 16:
         return 16.0
     return bits + 32.0 / group

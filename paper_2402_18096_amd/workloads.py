@@ -60,6 +60,7 @@ class Workload:
     q_outlier_scale: float
     seed: int
     head_dim: int = HEAD_DIM
+    key_block: int = 0    # 0: per-token keys; 64: retained keys per channel over 64-position blocks
 
     @property
     def group_size(self) -> int:
