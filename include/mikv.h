@@ -53,7 +53,10 @@ enum mikv_status {
 /* Bits of mikv_cache.status, set on the device. */
 enum mikv_device_error {
   MIKV_DEVERR_HI_FULL = 1, /* importance pool overflow: token not stored */
-  MIKV_DEVERR_LO_FULL = 2  /* retained pool overflow: token not stored */
+  MIKV_DEVERR_LO_FULL = 2, /* retained pool overflow: token not stored */
+  MIKV_DEVERR_KEY_BLOCK = 4 /* key_block 64: a token for the retained pool whose key block is not
+                               complete, or a completed block with a key outside the importance
+                               pool (token or block parameters not stored) */
 };
 
 /* Flags of mikv_decode_attention. */
@@ -97,6 +100,20 @@ enum mikv_attention_flags {
  * status: one device int32 (required), see mikv_device_error.
  * Retained-pool tokens carry no score: they are never promoted again, so
  * their score would never be read.
+ *
+ * Per-channel key quantization (Appendix C, Table 6): key_block 64 quantizes
+ * the retained pool's keys per channel over blocks of 64 consecutive
+ * positions instead of per token (values stay per token).  The parameters of
+ * block b = positions [64 b, 64 b + 64) are Eq. 1 over the block's 64 keys,
+ * channel by channel, taken when the block is complete (from the keys given
+ * to mikv_quantize_kv, or from the importance pool when the block completes
+ * during decoding: with a window of at least 64 positions every key of an
+ * incomplete block is still there):
+ *   lo_kb fp16 (alpha, beta) pairs [NH, max_len / 64, 128, 2];
+ * a retained key's codes (lo_k, packed as before) are Eq. 1 of its fp16 key
+ * with its block's parameters of each channel; lo_kp is unused (may be
+ * NULL).  Requires hi_bits 16, lo_bits 2, 3 or 4, one query head per KV
+ * head, no balancer, and a window of at least 64 in the re-rank.
  */
 typedef struct mikv_cache {
   int32_t batch;
@@ -120,6 +137,8 @@ typedef struct mikv_cache {
   int32_t *n_lo;
   uint8_t *map;
   int32_t *status;
+  int32_t key_block;  /* 0: retained keys per token and channel group; 64: per channel and block of 64 positions */
+  uint16_t *lo_kb;    /* key_block 64: per-block key parameters (see above); else unused */
 } mikv_cache;
 
 /* Message describing the calling thread's last error ("" if none). */

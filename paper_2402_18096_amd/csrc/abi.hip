@@ -53,8 +53,16 @@ int validate_cache(const mikv_cache *c) {
     return set_error(MIKV_ERR_INVALID_ARG,
                      "cap_lo must be a multiple of 32 for a 2-bit retained pool shared by query heads (got %d)",
                      c->cap_lo);
+  if (c->key_block != 0 && c->key_block != kKeyBlock)
+    return set_error(MIKV_ERR_UNSUPPORTED, "key_block must be 0 or %d (got %d)", kKeyBlock, c->key_block);
+  if (c->key_block) {
+    if (c->hi_bits != 16 || (c->lo_bits != 2 && c->lo_bits != 3 && c->lo_bits != 4) || G != 1)
+      return set_error(MIKV_ERR_UNSUPPORTED,
+                       "per-channel keys need hi_bits 16, lo_bits 2, 3 or 4 and one query head per KV head");
+    if (!c->lo_kb) return set_error(MIKV_ERR_INVALID_ARG, "key_block %d needs lo_kb", c->key_block);
+  }
   if (!c->hi_k || !c->hi_v || !c->hi_pos || !c->hi_acc || !c->n_hi || !c->n_lo || !c->status ||
-      (!evicting(c) && (!c->lo_k || !c->lo_v || !c->lo_kp || !c->lo_vp || !c->lo_pos)))
+      (!evicting(c) && (!c->lo_k || !c->lo_v || (!c->lo_kp && !c->key_block) || !c->lo_vp || !c->lo_pos)))
     return set_error(MIKV_ERR_INVALID_ARG, "a required cache pointer is NULL");
   if (c->hi_bits != 16 && (!c->hi_kp || !c->hi_vp))
     return set_error(MIKV_ERR_INVALID_ARG, "hi_kp/hi_vp are required for an INT8 or INT4 importance pool");

@@ -84,6 +84,11 @@ struct AttnArgs {
   AppendArgs app;
   int hi_pending;
   int pool_major;  // dispatch every importance-pool chunk first (fp16 importance pools)
+  // per-channel retained keys (key_block 64): (alpha, beta) words
+  // [NH, n_kblk, 128] per key block, found through the token's position
+  const uint32_t *lo_kb;
+  const int32_t *lo_pos;
+  int n_kblk;
 };
 
 // Importance-pool tokens of head h, the pending new token included.
@@ -207,7 +212,7 @@ __device__ inline rsrc_t make_rsrc(const void *base, uint32_t bytes) {
 // WHICH: 1 the key segment and its group parameters, 2 the value's, 3 both.
 template <int BITS, int CPL, int WHICH = 3>
 __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, rsrc_t rkp, rsrc_t rvp, uint32_t orow,
-                                     uint32_t opar) {
+                                     uint32_t opar, uint32_t okp) {
   constexpr int KW = Rows<BITS, CPL>::KW;
   constexpr bool LK = (WHICH & 1) != 0, LV = (WHICH & 2) != 0;
   if constexpr (KW >= 4) {
@@ -247,12 +252,16 @@ __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, r
     if constexpr (LV) r.v[0] = __builtin_amdgcn_raw_buffer_load_b32(rv, orow, 0, 0);
   }
   if constexpr (BITS != 16) {
-    if constexpr (LK) r.kp = __builtin_amdgcn_raw_buffer_load_b32(rkp, opar, 0, 0);
+    if constexpr (LK) r.kp = __builtin_amdgcn_raw_buffer_load_b32(rkp, okp, 0, 0);
     if constexpr (LV) r.vp = __builtin_amdgcn_raw_buffer_load_b32(rvp, opar, 0, 0);
   }
 }
 
-template <int BITS, int G, int CPL, bool SPLITQ, int UNROLL, int PREFETCH>
+// KPC: retained keys quantized per channel over 64-position blocks
+// (Appendix C).  The key's "parameter" word is then its position; a lane
+// keeps q_c * alpha_c (times the code class factor) and sum_c q_c beta_c for
+// the block of its current token and refreshes them when the block changes.
+template <int BITS, int G, int CPL, bool SPLITQ, int UNROLL, int PREFETCH, bool KPC = false>
 __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, bool is_hi, float *s_lds) {
   using F = Fmt<BITS>;
   constexpr int LPT = kHeadDim / CPL, TPW = 64 / LPT, NP = CPL / 2;
@@ -307,11 +316,13 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   // fixed per iteration and the unroll steps are immediate offsets.
   const rsrc_t rk = make_rsrc(kb, (uint32_t)n_pool * (uint32_t)kRow);
   const rsrc_t rv = make_rsrc(vb, (uint32_t)n_pool * (uint32_t)kRow);
-  const rsrc_t rkp = make_rsrc(Q ? (const void *)kpb : (const void *)kb, Q ? (uint32_t)n_pool * ng * 4u : 0u);
+  const rsrc_t rkp = KPC ? make_rsrc(A.lo_pos + (int64_t)h * cap, (uint32_t)n_pool * 4u)
+                         : make_rsrc(Q ? (const void *)kpb : (const void *)kb, Q ? (uint32_t)n_pool * ng * 4u : 0u);
   const rsrc_t rvp = make_rsrc(Q ? (const void *)vpb : (const void *)vb, Q ? (uint32_t)n_pool * ng * 4u : 0u);
   const uint32_t lane_tok = (uint32_t)(start + wave * TPW * UNROLL + tsub);
   const uint32_t off_row0 = lane_tok * (uint32_t)kRow + (uint32_t)(part * kSeg);
   const uint32_t off_par0 = (lane_tok * (uint32_t)ng + (uint32_t)g_lane) * 4u;
+  const uint32_t off_kp0 = KPC ? lane_tok * 4u : off_par0;
 
   // With `live` false the loads go through empty descriptors: they return
   // zero without a memory access, so a load needs no branch around it.
@@ -319,12 +330,15 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   auto load_part = [&](auto which, Rows<BITS, CPL>(&r)[UNROLL], int it, bool live = true) {
     const uint32_t orow = off_row0 + (uint32_t)(it * kPerIter) * (uint32_t)kRow;
     const uint32_t opar = off_par0 + (uint32_t)(it * kPerIter) * (uint32_t)ng * 4u;
+    const uint32_t okp = KPC ? off_kp0 + (uint32_t)(it * kPerIter) * 4u : opar;
     const rsrc_t ak = live ? rk : r_none, av = live ? rv : r_none;
     const rsrc_t akp = live ? rkp : r_none, avp = live ? rvp : r_none;
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
       load_seg_rows<BITS, CPL, decltype(which)::value>(r[u], ak, av, akp, avp, orow + (uint32_t)(u * TPW * kRow),
-                                                       opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u);
+                                                       opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u,
+                                                       KPC ? okp + (uint32_t)(u * TPW) * 4u
+                                                           : opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u);
   };
   auto load_it = [&](Rows<BITS, CPL>(&r)[UNROLL], int it) { load_part(std::integral_constant<int, 3>{}, r, it); };
 
@@ -343,6 +357,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   // stream starts one memory round trip after the wave does.
   half2_t qh[G][NP], ql[G][SPLITQ ? NP : 1];
   float qsum24[G];  // 2^-24 * sum of the lane's query channels
+  float qkeep[KPC ? G : 1][KPC ? CPL : 1];  // KPC: the lane's query channels (fp32)
   uint4 qraw[G][CPL / 8];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
@@ -379,6 +394,10 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
       for (int c = 0; c < CPL; ++c) qf[c] = qf[c] / bal[c];
     }
     auto qhat = [&](int c) { return qf[c]; };
+    if constexpr (KPC) {
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) qkeep[i][c] = qf[c];
+    }
     float s = 0.0f;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) s += qhat(c);
@@ -401,6 +420,41 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 #pragma unroll
   for (int i = 0; i < G; ++i) score_row[i] = scores ? scores + (int64_t)(qh0 + i) * cap : nullptr;
 
+  // KPC: q_c * alpha_c * 2^-cls (qa) and 2^-24 sum_c q_c beta_c (b24) of
+  // the lane's channels for key block kblk
+  float qa[KPC ? G : 1][KPC ? CPL : 1], b24[KPC ? G : 1];
+  int kblk = -1;
+  const rsrc_t rkb = KPC ? make_rsrc(A.lo_kb + ((int64_t)h * A.n_kblk) * kHeadDim, (uint32_t)A.n_kblk * kHeadDim * 4u)
+                         : r_none;
+  auto kpc_refresh = [&](int blk) {
+    if constexpr (KPC) {
+      uint32_t pw[CPL];
+#pragma unroll
+      for (int j = 0; j < CPL / 4; ++j) {
+        auto w = __builtin_amdgcn_raw_buffer_load_b128(rkb, ((uint32_t)blk * kHeadDim + part * CPL + 4 * j) * 4u, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pw[4 * j + e] = w[e];
+      }
+#pragma unroll
+      for (int i = 0; i < G; ++i) {
+        float bs = 0.0f;
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+          const float sc = __builtin_ldexpf(1.0f, -F::cls(p));
+#pragma unroll
+          for (int side = 0; side < 2; ++side) {
+            const int c = side ? F::hi(p) : F::lo(p);
+            const float a = f16_to_f32((uint16_t)(pw[c] & 0xffffu)), b = f16_to_f32((uint16_t)(pw[c] >> 16));
+            qa[i][c] = (qkeep[i][c] * a) * sc;
+            bs = fmaf(qkeep[i][c], b, bs);
+          }
+        }
+        b24[i] = __builtin_ldexpf(bs, -24);
+      }
+      kblk = blk;
+    }
+  };
+
   float s2[UNROLL][G];
   // Scores of one iteration (and the lazy running-max update).
   auto proc_k = [&](Rows<BITS, CPL>(&cur)[UNROLL], int it) {
@@ -413,19 +467,36 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
       uint32_t kx[NP];
       F::template unpack<CPL>(cur[u].k, kx);
       const half2_t kab = as_h2(cur[u].kp);  // (alpha, beta) of the key group
+      if constexpr (KPC) {
+        // the token's key block (the parameter word is its position); tokens
+        // past the pool read position 0 and are masked below
+        const int blk = min(max((int)cur[u].kp / kKeyBlock, 0), max(A.n_kblk - 1, 0));
+        if (blk != kblk) kpc_refresh(blk);
+      }
 #pragma unroll
       for (int i = 0; i < G; ++i) {
         float d = 0.0f;
+        if constexpr (KPC) {
+          // 2^-24 sum_c q_c alpha_c code_c: each masked code is an exact
+          // fp16 subnormal (code * 2^(cls - 24)) in a mixed-precision FMA
 #pragma unroll
-        for (int p = 0; p < NP; ++p) d = __builtin_amdgcn_fdot2(as_h2(kx[p]), qh[i][p], d, false);
-        if constexpr (SPLITQ) {
+          for (int p = 0; p < NP; ++p) {
+            const half2_t hk = as_h2(kx[p]);
+            d = fmaf(qa[i][F::lo(p)], (float)hk.x, d);
+            d = fmaf(qa[i][F::hi(p)], (float)hk.y, d);
+          }
+        } else {
 #pragma unroll
-          for (int p = 0; p < NP; ++p) d = __builtin_amdgcn_fdot2(as_h2(kx[p]), ql[i][p], d, false);
+          for (int p = 0; p < NP; ++p) d = __builtin_amdgcn_fdot2(as_h2(kx[p]), qh[i][p], d, false);
+          if constexpr (SPLITQ) {
+#pragma unroll
+            for (int p = 0; p < NP; ++p) d = __builtin_amdgcn_fdot2(as_h2(kx[p]), ql[i][p], d, false);
+          }
         }
         // 2^-24 (alpha * 2^24 * d + beta * qsum): the fp16 scale and zero
         // enter mixed-precision FMAs as stored; the power of two goes into
         // the final scale, so the result is the same bits
-        float s = Q ? fmaf((float)kab.x, d, fmaf((float)kab.y, qsum24[i], 0.0f)) : d;
+        float s = KPC ? d + b24[i] : Q ? fmaf((float)kab.x, d, fmaf((float)kab.y, qsum24[i], 0.0f)) : d;
         s = token_sum<LPT>(s) * s2scale_q;
         s = valid[u] ? s : kNegInf;
         s2[u][i] = s;
@@ -1077,7 +1148,7 @@ __device__ inline void append_in_chunk(const AttnArgs &A, int h, int chunk) {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-template <int HI, int LO, int G, bool SPLITQ>
+template <int HI, int LO, int G, bool SPLITQ, bool KPC = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
@@ -1110,6 +1181,8 @@ void attn_partial_kernel(AttnArgs A) {
   if (c < A.nc_hi) {
     if (A.hi_pending) append_in_chunk<HI>(A, h, c);
     attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
+  } else if constexpr (KPC) {
+    attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>(), true>(A, h, c - A.nc_hi, c, false, s_lds);
   } else if constexpr (LO == 2 && G >= 2) {
     __shared__ __align__(16) _Float16 w_lds[kWLds];  // value-MFMA weights, see w_index
     if (A.group == 32)
@@ -1511,6 +1584,9 @@ AttnArgs make_args(const mikv_cache *c, const Plan &p, const uint16_t *q, const 
   // the grid is shorter (measured: long_context -1.8 %, mistral_7b -2.3 % per
   // step; an INT8 pool gained nothing, llama2_7b lost 1.2 %)
   A.pool_major = c->hi_bits == 16 ? 1 : 0;
+  A.lo_kb = c->key_block ? (const uint32_t *)c->lo_kb : nullptr;
+  A.lo_pos = c->lo_pos;
+  A.n_kblk = c->key_block ? key_blocks_of(c) : 0;
   return A;
 }
 
@@ -1596,6 +1672,17 @@ int decode_partial(const mikv_cache *c, int32_t length, const uint16_t *q, const
   if (k_new) set_append(A, c, length, k_new, v_new, balance);
   dim3 grid((p.nc_hi + p.nc_lo) * n_heads_of(c));
   const int G = group_size_of(c);
+  if (c->key_block) {
+    // per-channel retained keys: fp16 importance pool, one query head per
+    // KV head, no balancer (validated)
+    if (balance) return set_error(MIKV_ERR_INVALID_ARG, "mikv_decode_attention: per-channel keys take no balancer");
+    switch (c->lo_bits) {
+      case 2: hipLaunchKernelGGL((attn_partial_kernel<16, 2, 1, false, true>), grid, dim3(64), 0, st, A); break;
+      case 3: hipLaunchKernelGGL((attn_partial_kernel<16, 3, 1, false, true>), grid, dim3(64), 0, st, A); break;
+      default: hipLaunchKernelGGL((attn_partial_kernel<16, 4, 1, false, true>), grid, dim3(64), 0, st, A); break;
+    }
+    return check_launch("mikv_decode_attention_partial");
+  }
   switch (format_key(c)) {
     case 1602: launch_partial_g<16, 2>(A, G, grid, st); break;
     case 1604: launch_partial_g<16, 4>(A, G, grid, st); break;

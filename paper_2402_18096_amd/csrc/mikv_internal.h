@@ -13,6 +13,7 @@
 namespace mikv {
 
 constexpr int kHeadDim = 128;
+constexpr int kKeyBlock = 64;  // positions per block of per-channel key parameters
 
 // ---------------------------------------------------------------------------
 // Host: error reporting.
@@ -52,6 +53,13 @@ inline bool evicting(const mikv_cache *c) { return c->lo_bits == 0; }
 // cache runs the 2-bit instantiation with its retained pool empty.
 inline int format_key(const mikv_cache *c) { return c->hi_bits * 100 + (evicting(c) ? 2 : c->lo_bits); }
 inline int n_heads_of(const mikv_cache *c) { return c->batch * c->kv_heads; }
+// Blocks of per-channel key parameters per head (key_block 64).
+inline int key_blocks_of(const mikv_cache *c) { return c->max_len / kKeyBlock; }
+
+// Per-channel key parameters of key block `blk` from the keys of its 64
+// positions in the importance pool (quantize.hip): the block completed
+// during decoding.  key_block caches only.
+int close_key_block_from_pool(const mikv_cache *c, int32_t blk, hipStream_t st);
 
 // Bytes of one token (key + value, codes + fp16 params) in a pool of `bits`.
 inline int64_t token_bytes(int bits, int group) {
@@ -177,6 +185,29 @@ __device__ inline void encode32(const float x[32], const GroupParams &p, uint32_
   for (int i = 0; i < BITS; ++i) w[i] = 0u;
 #pragma unroll
   for (int c = 0; c < 32; ++c) put_code<BITS>(w, c, (uint32_t)fminf(fmaxf(rintf(q[c]), 0.0f), top));
+}
+
+// Eq. 1 codes of the 32 channels [32 * lane4, 32 * lane4 + 32) of a key with
+// its block's per-channel parameters, packed LSB-first into w[BITS].
+template <int BITS>
+__device__ inline void encode_key_channels(const float x[32], const uint32_t *blk_par, int lane4, uint32_t w[BITS]) {
+#pragma unroll
+  for (int i = 0; i < BITS; ++i) w[i] = 0u;
+  const uint4 *p4 = reinterpret_cast<const uint4 *>(blk_par + lane4 * 32);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint4 pw = p4[j];
+    const uint32_t ws[4] = {pw.x, pw.y, pw.z, pw.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      GroupParams gp;
+      gp.a16 = (uint16_t)(ws[e] & 0xffffu);
+      gp.b16 = (uint16_t)(ws[e] >> 16);
+      gp.a = f16_to_f32(gp.a16);
+      gp.b = f16_to_f32(gp.b16);
+      put_code<BITS>(w, 4 * j + e, encode(x[4 * j + e], gp, BITS));
+    }
+  }
 }
 
 // c ? a : b for wave-uniform pointers (argument fields) and a per-lane

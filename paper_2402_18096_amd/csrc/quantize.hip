@@ -48,6 +48,9 @@ struct Pools {
   int cap_hi, cap_lo, max_len, group;
   int v_tiled;  // 2-bit values in the tiled layout (int2_values_tiled)
   int evict;    // no retained pool: tokens not placed in the importance pool are dropped
+  // per-channel keys: (alpha, beta) words [NH, n_kblk, 128] per key block
+  const uint32_t *lo_kb;
+  int n_kblk;
 };
 
 Pools make_pools(const mikv_cache *c) {
@@ -73,8 +76,83 @@ Pools make_pools(const mikv_cache *c) {
   p.group = c->group;
   p.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
   p.evict = evicting(c) ? 1 : 0;
+  p.lo_kb = c->key_block ? (const uint32_t *)c->lo_kb : nullptr;
+  p.n_kblk = c->key_block ? key_blocks_of(c) : 0;
   return p;
 }
+
+// Per-channel key quantization (Appendix C): Eq. 1 over the 64 keys of a
+// block, channel by channel.  Thread t takes channel t % 128 of half the
+// block's rows (t / 128); the halves combine in LDS.  `row_of(i)` gives the
+// fp16 row of the block's i-th position, or NULL when that key is missing
+// (then nothing is written and the status bit is set).
+template <class RowOf>
+__device__ inline void block_params(RowOf row_of, uint32_t *dst, int bits, int32_t *status) {
+  __shared__ float s_mn[kHeadDim], s_mx[kHeadDim];
+  __shared__ int s_missing;
+  const int c = threadIdx.x & (kHeadDim - 1), half = threadIdx.x >> 7;
+  if (threadIdx.x == 0) s_missing = 0;
+  __syncthreads();
+  float mn = __builtin_huge_valf(), mx = -__builtin_huge_valf();
+  for (int i = half * (kKeyBlock / 2); i < (half + 1) * (kKeyBlock / 2); ++i) {
+    const uint16_t *r = row_of(i);
+    if (!r) {
+      s_missing = 1;
+      continue;
+    }
+    const float x = f16_to_f32(r[c]);
+    mn = fminf(mn, x);
+    mx = fmaxf(mx, x);
+  }
+  if (half == 1) {
+    s_mn[c] = mn;
+    s_mx[c] = mx;
+  }
+  __syncthreads();
+  if (half == 0) {
+    if (s_missing) {
+      if (c == 0) atomicOr(status, MIKV_DEVERR_KEY_BLOCK);
+      return;
+    }
+    const GroupParams p = group_params(fminf(mn, s_mn[c]), fmaxf(mx, s_mx[c]), bits);
+    dst[c] = (uint32_t)p.a16 | ((uint32_t)p.b16 << 16);
+  }
+}
+
+// Blocks whose 64 positions all lie in the rows being placed: block
+// blockIdx.x of the range, head blockIdx.y; k is fp16 [NH, n, 128] for
+// positions pos0 .. pos0 + n - 1.
+__global__ __launch_bounds__(256) void key_block_rows_kernel(Pools P, const uint16_t *k, int pos0, int n, int blk0,
+                                                             int bits) {
+  const int h = blockIdx.y, blk = blk0 + blockIdx.x;
+  const int64_t first = (int64_t)blk * kKeyBlock - pos0;  // row of the block's first position
+  auto row_of = [&](int i) -> const uint16_t * { return k + ((int64_t)h * n + first + i) * kHeadDim; };
+  block_params(row_of, const_cast<uint32_t *>(P.lo_kb) + ((int64_t)h * P.n_kblk + blk) * kHeadDim, bits, P.status);
+}
+
+// A block completed during decoding: its keys are in the importance pool
+// (every position of it is in the recent window), found by position.
+__global__ __launch_bounds__(256) void key_block_pool_kernel(Pools P, int blk, int bits) {
+  const int h = blockIdx.x;
+  __shared__ int s_slot[kKeyBlock];
+  if (threadIdx.x < kKeyBlock) s_slot[threadIdx.x] = -1;
+  __syncthreads();
+  const int n = min(P.n_hi[h], P.cap_hi);
+  const int p0 = blk * kKeyBlock;
+  const int32_t *pos = P.hi_pos + (int64_t)h * P.cap_hi;
+  for (int i = threadIdx.x; i < n; i += 256) {
+    const int p = pos[i];
+    if (p >= p0 && p < p0 + kKeyBlock) s_slot[p - p0] = i;
+  }
+  __syncthreads();
+  const uint16_t *hk = reinterpret_cast<const uint16_t *>(P.hi_k) + (int64_t)h * P.cap_hi * kHeadDim;
+  auto row_of = [&](int i) -> const uint16_t * {
+    const int sl = s_slot[i];
+    return sl < 0 ? nullptr : hk + (int64_t)sl * kHeadDim;
+  };
+  block_params(row_of, const_cast<uint32_t *>(P.lo_kb) + ((int64_t)h * P.n_kblk + blk) * kHeadDim, bits, P.status);
+}
+
 
 __host__ __device__ inline AppendArgs append_args(const Pools &P, const uint16_t *k, const uint16_t *v,
                                                   const float *balance, int pos, const float *score_init) {
@@ -180,6 +258,12 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
     int cap = is_hi ? P.cap_hi : P.cap_lo;
     if (!is_hi && P.evict) {
       slot = -1;  // evicted: stored nowhere (the map says "not in the importance pool")
+    } else if (!is_hi && P.lo_kb &&
+               ((pos0 + j) / kKeyBlock * kKeyBlock < pos0 || (pos0 + j) / kKeyBlock * kKeyBlock + kKeyBlock > pos0 + n)) {
+      // a retained key needs its block's parameters: the block must lie
+      // within the placed positions
+      atomicOr(P.status, MIKV_DEVERR_KEY_BLOCK);
+      slot = -1;
     } else if (slot >= cap) {
       atomicOr(P.status, is_hi ? MIKV_DEVERR_HI_FULL : MIKV_DEVERR_LO_FULL);
       slot = -1;
@@ -247,6 +331,18 @@ __global__ __launch_bounds__(256) void place_kernel(Pools P, const uint16_t *k, 
           P.lo_vp[((int64_t)h * P.cap_lo + sl) * ng + (lane4 * 32) / P.group] =
               (uint32_t)gp.a16 | ((uint32_t)gp.b16 << 16);
       }
+    } else if (!is_v && P.lo_kb) {
+      // per-channel key: codes with its block's parameters (the block is
+      // complete: the placement below refused tokens of incomplete blocks)
+      if (store) {
+        uint32_t w[LO_BITS];
+        const int blk = (pos0 + j0 + t) / kKeyBlock;
+        encode_key_channels<LO_BITS>(x, P.lo_kb + ((int64_t)h * P.n_kblk + blk) * kHeadDim, lane4, w);
+        uint32_t *dst = reinterpret_cast<uint32_t *>(P.lo_k + ((int64_t)h * P.cap_lo + sl) * (kHeadDim * LO_BITS / 8) +
+                                                     lane4 * (32 * LO_BITS / 8));
+#pragma unroll
+        for (int i = 0; i < LO_BITS; ++i) dst[i] = w[i];
+      }
     } else {
       uint8_t *dst = (is_v ? P.lo_v : P.lo_k) + ((int64_t)h * P.cap_lo + sl) * (kHeadDim * LO_BITS / 8) +
                      lane4 * (32 * LO_BITS / 8);
@@ -309,6 +405,13 @@ void launch_place(const mikv_cache *c, const uint16_t *k, const uint16_t *v, con
     return;
   }
   int nchunks = (n + kChunk - 1) / kChunk;
+  if (P.lo_kb) {
+    // parameters of the key blocks that lie within the placed positions,
+    // before the retained keys are encoded with them
+    const int b0 = (pos0 + kKeyBlock - 1) / kKeyBlock, b1 = (pos0 + n) / kKeyBlock;
+    if (b1 > b0)
+      hipLaunchKernelGGL(key_block_rows_kernel, dim3(b1 - b0, NH), dim3(256), 0, st, P, k, pos0, n, b0, LO_BITS);
+  }
   if (hi_mask) {
     hipLaunchKernelGGL(count_hi_kernel, dim3(nchunks, NH), dim3(kChunk), 0, st, hi_mask, n, nchunks, counts);
   }
@@ -322,6 +425,13 @@ void launch_place(const mikv_cache *c, const uint16_t *k, const uint16_t *v, con
 }
 
 }  // namespace
+
+int close_key_block_from_pool(const mikv_cache *c, int32_t blk, hipStream_t st) {
+  if (!c->key_block || blk < 0 || blk >= key_blocks_of(c)) return MIKV_OK;
+  hipLaunchKernelGGL(key_block_pool_kernel, dim3(n_heads_of(c)), dim3(256), 0, st, make_pools(c), (int)blk,
+                     (int)c->lo_bits);
+  return check_launch("key block parameters");
+}
 
 }  // namespace mikv
 
@@ -384,6 +494,8 @@ extern "C" int mikv_quantize_kv(const mikv_cache *c, const uint16_t *k, const ui
       return set_error(MIKV_ERR_CAPACITY, "mikv_quantize_kv: workspace too small (%zu < %zu)", workspace_bytes,
                        mikv_quantize_workspace_size(c, n));
   }
+  if (c->key_block && balance)
+    return set_error(MIKV_ERR_INVALID_ARG, "mikv_quantize_kv: per-channel keys take no balancer");
   hipStream_t st = (hipStream_t)stream;
   int32_t *counts = (int32_t *)workspace;
   switch (format_key(c)) {
@@ -397,5 +509,11 @@ extern "C" int mikv_quantize_kv(const mikv_cache *c, const uint16_t *k, const ui
     case 804: launch_place<8, 4>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
     default: launch_place<8, 8>(c, k, v, balance, pos0, n, hi_mask, score_init, counts, st); break;
   }
-  return check_launch("mikv_quantize_kv");
+  rc = check_launch("mikv_quantize_kv");
+  if (rc || !c->key_block) return rc;
+  // a key block that started before pos0 and is complete now: its
+  // parameters from the importance pool, where its keys are
+  const int b = pos0 / kKeyBlock;
+  if (pos0 % kKeyBlock != 0 && (b + 1) * kKeyBlock <= pos0 + n) return close_key_block_from_pool(c, b, st);
+  return MIKV_OK;
 }

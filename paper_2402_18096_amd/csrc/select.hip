@@ -114,6 +114,9 @@ int select_topk(const mikv_cache *c, int32_t length, int32_t k_heavy, int32_t wi
                      "mikv_select_topk: length %d outside [1, max_len]", length);
   if (!ws || ws_bytes < mikv_select_workspace_size(c))
     return set_error(MIKV_ERR_CAPACITY, "mikv_select_topk: workspace too small");
+  if (c->key_block && window < kKeyBlock)
+    return set_error(MIKV_ERR_INVALID_ARG, "mikv_select_topk: per-channel keys need a window >= %d (got %d)",
+                     kKeyBlock, window);
   SelArgs A = make_sel_args(c, length, k_heavy, window, ws);
   A.pending = appended ? 1 : 0;
   const int NH = n_heads_of(c);

@@ -137,6 +137,9 @@ struct SelArgs {
   int v_tiled;  // 2-bit values in the tiled layout (int2_values_tiled)
   int pending;  // n_hi does not yet count the step's appended token (slot n_hi holds it)
   int evict;    // no retained pool: a token that leaves the importance pool is dropped
+  // per-channel keys: (alpha, beta) words [NH, n_kblk, 128] per key block
+  const uint32_t *lo_kb;
+  int n_kblk;
 };
 
 // Decode the 32 channels [part*32, part*32+32) of an importance-pool row.
@@ -202,9 +205,18 @@ __device__ inline GroupParams lo_words(const SelArgs &A, const float x[32], uint
 // codes token-major, except 2-bit values of a GQA cache (tiled layout).
 template <int LO_BITS>
 __device__ inline void store_lo_segment(const SelArgs &A, int h, int64_t lslot, bool is_v, int part,
-                                        const float x[32]) {
+                                        const float x[32], int pos) {
   const int ng = kHeadDim / A.group;
   uint32_t w[LO_BITS];
+  if (!is_v && A.lo_kb) {
+    // per-channel key: its block's parameters (the block is complete: the
+    // token has left a window of at least one block)
+    encode_key_channels<LO_BITS>(x, A.lo_kb + ((int64_t)h * A.n_kblk + pos / kKeyBlock) * kHeadDim, part, w);
+    uint32_t *codes = reinterpret_cast<uint32_t *>(A.lo_k + lslot * (kHeadDim * LO_BITS / 8) + part * (32 * LO_BITS / 8));
+#pragma unroll
+    for (int i = 0; i < LO_BITS; ++i) codes[i] = w[i];
+    return;
+  }
   GroupParams p = lo_words<LO_BITS>(A, x, w);
   if (LO_BITS == 2 && is_v && A.v_tiled) {
     store_int2_v(A.lo_v + (int64_t)h * A.cap_lo * (kHeadDim / 4), lslot - (int64_t)h * A.cap_lo, part, w);
@@ -228,7 +240,7 @@ __device__ inline void demote_row(const SelArgs &A, int h, int slot, int64_t lsl
   const uint32_t *pars = HI_BITS == 16 ? nullptr : lane_pick(is_v, A.hi_vp, A.hi_kp) + (int64_t)h * A.cap_hi * ng;
   float x[32];
   load_hi_segment<HI_BITS>(A, rows, pars, slot, part, x);
-  store_lo_segment<LO_BITS>(A, h, lslot, is_v, part, x);
+  store_lo_segment<LO_BITS>(A, h, lslot, is_v, part, x, p);
   if (threadIdx.x == 0) {
     A.lo_pos[lslot] = p;
     if (A.map) A.map[(int64_t)h * A.max_len + p] = 0;
@@ -397,7 +409,7 @@ __device__ __attribute__((always_inline)) void select_finish(const SelArgs &A, i
     float x[32];
     load_hi_segment<HI_BITS>(A, rows, pars, slot, part, x);
     const int64_t lslot = (int64_t)h * A.cap_lo + n_lo0 + d;
-    store_lo_segment<LO_BITS>(A, h, lslot, is_v, part, x);
+    store_lo_segment<LO_BITS>(A, h, lslot, is_v, part, x, pos[slot]);
     if (part == 0 && !is_v) {
       const int p = pos[slot];
       A.lo_pos[lslot] = p;
@@ -482,6 +494,8 @@ inline SelArgs make_sel_args(const mikv_cache *c, int length, int k_heavy, int w
   A.v_tiled = int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) ? 1 : 0;
   A.pending = 0;
   A.evict = evicting(c) ? 1 : 0;
+  A.lo_kb = c->key_block ? (const uint32_t *)c->lo_kb : nullptr;
+  A.n_kblk = c->key_block ? key_blocks_of(c) : 0;
   return A;
 }
 

@@ -41,6 +41,13 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
   const bool fused = (flags & MIKV_ATTN_ACCUMULATE) != 0;
   if (!fused && !probs_hi)
     return set_error(MIKV_ERR_INVALID_ARG, "mikv_decode_step: probs_hi is required unless MIKV_ATTN_ACCUMULATE");
+  if (c->key_block && (balance || window < kKeyBlock))
+    return set_error(MIKV_ERR_INVALID_ARG, "mikv_decode_step: per-channel keys need no balancer and a window >= %d",
+                     kKeyBlock);
+  // the new token (position length - 1) completes a key block: its
+  // per-channel parameters are taken at the end of the step, from the
+  // importance pool (the fused paths append inside the attention)
+  const int close_blk = c->key_block && fused && length % kKeyBlock == 0 ? length / kKeyBlock - 1 : -1;
   const size_t need = mikv_decode_step_workspace_size(c, length);
   if (!workspace || workspace_bytes < need)
     return set_error(MIKV_ERR_CAPACITY, "mikv_decode_step: workspace too small (%zu < %zu)", workspace_bytes, need);
@@ -61,6 +68,7 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
     rc = decode_finalize_select(c, length, q, balance, scale, out, probs_hi, probs_lo, ws, attn_ws, k_heavy, window,
                                 ws + attn_ws, true, st);
     if (rc) return rc;
+    if (close_blk >= 0 && (rc = close_key_block_from_pool(c, close_blk, st))) return rc;
     mark(3);
     mark(4);
     mark(5);
@@ -79,6 +87,7 @@ extern "C" int mikv_decode_step(const mikv_cache *c, int32_t length, const uint1
     mark(4);
     rc = select_topk(c, length, k_heavy, window, ws + attn_ws, workspace_bytes - attn_ws, true, st);
     if (rc) return rc;
+    if (close_blk >= 0 && (rc = close_key_block_from_pool(c, close_blk, st))) return rc;
     mark(5);
     return MIKV_OK;
   }

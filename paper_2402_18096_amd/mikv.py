@@ -27,6 +27,7 @@ HEAD_DIM = 128
 ATTN_ACCUMULATE = 1
 DEVERR_HI_FULL = 1
 DEVERR_LO_FULL = 2
+DEVERR_KEY_BLOCK = 4
 
 
 class MikvError(RuntimeError):
@@ -38,7 +39,8 @@ class CacheDesc(ctypes.Structure):
     _fields_ = [(n, c_int32) for n in ("batch", "q_heads", "kv_heads", "head_dim", "group", "hi_bits",
                                        "lo_bits", "cap_hi", "cap_lo", "max_len")] + \
                [(n, c_void_p) for n in ("hi_k", "hi_v", "hi_kp", "hi_vp", "hi_pos", "hi_acc", "n_hi",
-                                        "lo_k", "lo_v", "lo_kp", "lo_vp", "lo_pos", "n_lo", "map", "status")]
+                                        "lo_k", "lo_v", "lo_kp", "lo_vp", "lo_pos", "n_lo", "map", "status")] + \
+               [("key_block", c_int32), ("lo_kb", c_void_p)]
 
 
 _LIB = None
@@ -135,7 +137,7 @@ class MikvCache:
     (capacity 0) and tokens that leave the importance pool are dropped."""
 
     def __init__(self, batch: int, q_heads: int, kv_heads: int, group: int, hi_bits: int, lo_bits: int,
-                 cap_hi: int, cap_lo: int, max_len: int, device="cuda", with_map: bool = True):
+                 cap_hi: int, cap_lo: int, max_len: int, device="cuda", with_map: bool = True, key_block: int = 0):
         self.values_tiled = lo_bits == 2 and q_heads >= 2 * kv_heads
         if lo_bits == 0:
             cap_lo = 0
@@ -159,7 +161,11 @@ class MikvCache:
         self.n_hi = z(NH, dt=torch.int32)
         row = D * lo_bits // 8
         self.lo_k, self.lo_v = z(NH, cap_lo, row, dt=torch.uint8), z(NH, cap_lo, row, dt=torch.uint8)
-        self.lo_kp, self.lo_vp = z(NH, cap_lo, ng, 2, dt=torch.int16), z(NH, cap_lo, ng, 2, dt=torch.int16)
+        # per-token key parameters, or (key_block 64) per-block, per-channel ones
+        self.key_block = key_block
+        self.lo_kp = None if key_block else z(NH, cap_lo, ng, 2, dt=torch.int16)
+        self.lo_vp = z(NH, cap_lo, ng, 2, dt=torch.int16)
+        self.lo_kb = z(NH, max(1, max_len // key_block), D, 2, dt=torch.int16) if key_block else None
         self.lo_pos = z(NH, cap_lo, dt=torch.int32)
         self.n_lo = z(NH, dt=torch.int32)
         self.map = z(NH, max_len, dt=torch.uint8) if with_map else None
@@ -168,7 +174,8 @@ class MikvCache:
         self.desc = CacheDesc(batch, q_heads, kv_heads, D, group, hi_bits, lo_bits, cap_hi, cap_lo, max_len,
                               p(self.hi_k), p(self.hi_v), p(self.hi_kp), p(self.hi_vp), p(self.hi_pos),
                               p(self.hi_acc), p(self.n_hi), p(self.lo_k), p(self.lo_v), p(self.lo_kp),
-                              p(self.lo_vp), p(self.lo_pos), p(self.n_lo), p(self.map), p(self.status))
+                              p(self.lo_vp), p(self.lo_pos), p(self.n_lo), p(self.map), p(self.status),
+                              key_block, p(self.lo_kb))
 
     @property
     def n_heads(self) -> int:
@@ -183,7 +190,12 @@ class MikvCache:
         def tb(bits):
             if bits == 0:  # evicted tokens are not stored
                 return 0
-            return 4 * HEAD_DIM if bits == 16 else 2 * (HEAD_DIM * bits // 8 + 4 * (HEAD_DIM // self.group))
+            if bits == 16:
+                return 4 * HEAD_DIM
+            codes = HEAD_DIM * bits // 8
+            if self.key_block:  # key: codes + its share of the block's per-channel (alpha, beta)
+                return codes + 4 * HEAD_DIM // self.key_block + codes + 4 * (HEAD_DIM // self.group)
+            return 2 * (codes + 4 * (HEAD_DIM // self.group))
         return self.n_heads * (n_hi * tb(self.hi_bits) + (length - n_hi) * tb(self.lo_bits))
 
 
@@ -378,7 +390,7 @@ class MikvDecoder:
         cap_hi = min(self.max_len, heavy_budget(self.max_len, wl.ratio_num, wl.ratio_den, wl.window,
                                                 wl.window_in_ratio) + wl.window + cap_slack)
         self.cache = MikvCache(wl.batch, wl.q_heads, wl.kv_heads, wl.group, wl.hi_bits, wl.lo_bits, cap_hi,
-                               self.max_len, self.max_len, device)
+                               self.max_len, self.max_len, device, key_block=wl.key_block)
         c = self.cache
         self.length = 0
         self.balance = None

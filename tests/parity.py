@@ -61,12 +61,13 @@ def gather_gpu_state(c: mikv.MikvCache):
     lk, lv = c.lo_k.cpu().numpy(), c.lo_v.cpu().numpy()
     if c.values_tiled:
         lv = int2_values_token_major(lv, c.cap_lo)
-    lkp = c.lo_kp.cpu().numpy().view(np.uint16)
+    lkp = c.lo_kp.cpu().numpy().view(np.uint16) if c.lo_kp is not None else None
     lvp = c.lo_vp.cpu().numpy().view(np.uint16)
+    lkb = c.lo_kb.cpu().numpy().view(np.uint16) if c.lo_kb is not None else None
     hkp = c.hi_kp.cpu().numpy().view(np.uint16) if c.hi_kp is not None else None
     hvp = c.hi_vp.cpu().numpy().view(np.uint16) if c.hi_vp is not None else None
     return dict(n_hi=n_hi, n_lo=n_lo, hi_pos=hi_pos, lo_pos=lo_pos, hk=hk, hv=hv, acc=acc, lk=lk, lv=lv, lkp=lkp,
-                lvp=lvp, hkp=hkp, hvp=hvp, map=None if c.map is None else c.map.cpu().numpy())
+                lvp=lvp, hkp=hkp, hvp=hvp, lkb=lkb, map=None if c.map is None else c.map.cpu().numpy())
 
 
 def compare_state(c: mikv.MikvCache, orc: oracle.OracleCache, heads=None, tag=""):
@@ -106,8 +107,15 @@ def compare_state(c: mikv.MikvCache, orc: oracle.OracleCache, heads=None, tag=""
             continue
         np.testing.assert_array_equal(s["lk"][gh, :nl], oracle.pack(orc.lk[oh, lp], bits), err_msg=f"{tag} lo K codes")
         np.testing.assert_array_equal(s["lv"][gh, :nl], oracle.pack(orc.lv[oh, lp], bits), err_msg=f"{tag} lo V codes")
-        np.testing.assert_array_equal(s["lkp"][gh, :nl, :, 0], orc.lk_a[oh, lp], err_msg=f"{tag} lo K alpha")
-        np.testing.assert_array_equal(s["lkp"][gh, :nl, :, 1], orc.lk_b[oh, lp], err_msg=f"{tag} lo K beta")
+        if orc.key_block:
+            # per-channel key parameters of every complete block
+            nb = int(orc.kb_done[oh].sum())
+            assert orc.kb_done[oh, :nb].all()
+            np.testing.assert_array_equal(s["lkb"][gh, :nb, :, 0], orc.kb_a[oh, :nb], err_msg=f"{tag} key block alpha")
+            np.testing.assert_array_equal(s["lkb"][gh, :nb, :, 1], orc.kb_b[oh, :nb], err_msg=f"{tag} key block beta")
+        else:
+            np.testing.assert_array_equal(s["lkp"][gh, :nl, :, 0], orc.lk_a[oh, lp], err_msg=f"{tag} lo K alpha")
+            np.testing.assert_array_equal(s["lkp"][gh, :nl, :, 1], orc.lk_b[oh, lp], err_msg=f"{tag} lo K beta")
         np.testing.assert_array_equal(s["lvp"][gh, :nl, :, 0], orc.lv_a[oh, lp], err_msg=f"{tag} lo V alpha")
         np.testing.assert_array_equal(s["lvp"][gh, :nl, :, 1], orc.lv_b[oh, lp], err_msg=f"{tag} lo V beta")
 
@@ -133,7 +141,8 @@ class Lockstep:
         self.k, self.v, self.sc, self.qp, self.q, self.kn, self.vn = inputs(wl, steps)
         self.dec = mikv.MikvDecoder(wl, max_len=max_len or wl.context + steps, device="cuda", fused=fused)
         NH, G = wl.n_heads, wl.group_size
-        self.orc = oracle.OracleCache(NH, G, self.dec.max_len, wl.hi_bits, wl.lo_bits, wl.group)
+        self.orc = oracle.OracleCache(NH, G, self.dec.max_len, wl.hi_bits, wl.lo_bits, wl.group,
+                                      key_block=wl.key_block)
         self.bal = None
 
     def prefill(self):
@@ -224,7 +233,8 @@ class SampledLockstep:
         self.qp_s = np16(qp.reshape(NH, G, T, 128).index_select(0, sel)) if qp is not None else None
         self.dec.prefill(k, v, sc, qp)
         del k, v, qp
-        self.orc = oracle.OracleCache(len(self.heads), G, self.dec.max_len, wl.hi_bits, wl.lo_bits, wl.group)
+        self.orc = oracle.OracleCache(len(self.heads), G, self.dec.max_len, wl.hi_bits, wl.lo_bits, wl.group,
+                                      key_block=wl.key_block)
         self.bal = None
 
     def prefill(self):

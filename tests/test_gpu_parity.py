@@ -366,6 +366,68 @@ def test_full_size_int3_retained_sampled_heads():
     torch.cuda.empty_cache()
 
 
+# -- per-channel key quantization (Appendix C) -------------------------------------
+
+def _channel_keys(name, **kw):
+    """A workload with the retained keys quantized per channel over 64-position
+    blocks: fp16 importance cache, no balancer (the per-channel quantizer
+    replaces it, Table 6)."""
+    return workloads.small_workload(name, **kw).with_(hi_bits=16, balanced=False, key_block=64)
+
+
+@pytest.mark.parametrize("name,shape", [
+    ("long_context", dict(batch=1, q_heads=3, kv_heads=3, context=4090)),     # a block completes at step 5
+    ("llama2_13b", dict(batch=2, q_heads=3, kv_heads=3, context=1725)),       # Student-t keys, INT2 g32, W 64
+    ("long_context", dict(batch=1, q_heads=2, kv_heads=2, context=2000, lo_bits=3)),
+    ("llama2_7b", dict(batch=1, q_heads=2, kv_heads=2, context=1500, lo_bits=4)),
+])
+@pytest.mark.parametrize("fused", [False, True])
+def test_lockstep_per_channel_keys(name, shape, fused):
+    """Per-channel key blocks through prefill (parameters from the prompt),
+    decode steps (a block completing from the importance pool), attention
+    over per-channel retained keys and per-token demotion codes: bit-exact
+    state including every block's parameters, o and p within tolerance."""
+    _dev()
+    wl = _channel_keys(name, **shape)
+    run = Lockstep(wl, 8, fused=fused)
+    run.prefill()
+    for t in range(8):
+        run.step(t)
+
+
+def test_lockstep_per_channel_keys_demote_from_decoded_blocks():
+    """Long enough (W = 64, 100 steps) that blocks completed during decoding
+    lose tokens to the retained pool, whose keys then take those blocks'
+    parameters; the many-demotion path runs on the last steps."""
+    _dev()
+    wl = _channel_keys("long_context", batch=1, q_heads=2, kv_heads=2, context=700, window=64)
+    run = Lockstep(wl, 100, fused=True)
+    run.prefill()
+    for t in range(100):
+        if t == 96:
+            run.wl = wl.with_(ratio_den=14)        # budget drops: several demotions per head
+            run.dec.wl = run.wl
+        run.step(t, check_state=t % 8 == 7 or t >= 96)
+    nb = run.orc.kb_done.sum(1)
+    assert (nb == (700 + 100) // 64).all()
+
+
+@pytest.mark.parametrize("name", ["long_context", "llama2_13b"])
+def test_full_size_per_channel_keys_sampled_heads(name):
+    """Per-channel keys at the full long_context and 13B shapes in the
+    benchmark's launch configuration, the oracle following three heads."""
+    _dev()
+    wl = workloads.WORKLOADS[name].with_(hi_bits=16, balanced=False, key_block=64)
+    NH = wl.n_heads
+    print(f"[full-size per-channel keys] {name}: {NH} heads, 2 steps", flush=True)
+    run = SampledLockstep(wl, 2, heads=[0, NH // 2 + 1, NH - 1])
+    run.prefill()
+    for t in range(2):
+        run.step(t)
+    del run
+    torch.cuda.empty_cache()
+
+
 def test_capacity_overflow_sets_status_without_writing_out_of_bounds():
     dev = _dev()
     c = mikv.MikvCache(1, 2, 2, 32, 16, 2, cap_hi=4, cap_lo=32, max_len=64, device=dev)
