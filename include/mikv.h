@@ -122,7 +122,7 @@ typedef struct mikv_cache {
   int32_t head_dim;   /* 128 */
   int32_t group;      /* quantization group size: 32, 64 or 128 channels */
   int32_t hi_bits;    /* 16 (fp16), 8 (INT8) or 4 (INT4, with lo_bits 2 or 0) */
-  int32_t lo_bits;    /* 2, 3 (q_heads / kv_heads <= 2), 4 or 8; 0 = evict instead of retaining (see above) */
+  int32_t lo_bits;    /* 2, 3, 4 or 8; 0 = evict instead of retaining (see above) */
   int32_t cap_hi;     /* importance-pool slots per head */
   int32_t cap_lo;     /* retained-pool slots per head (ignored when lo_bits is 0) */
   int32_t max_len;    /* positions per head (length of map rows) */

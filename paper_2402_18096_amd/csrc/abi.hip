@@ -45,8 +45,6 @@ int validate_cache(const mikv_cache *c) {
     return set_error(MIKV_ERR_UNSUPPORTED, "an INT4 importance pool needs lo_bits 2 or 0 (got %d)", c->lo_bits);
   if (c->lo_bits != 0 && c->lo_bits != 2 && c->lo_bits != 3 && c->lo_bits != 4 && c->lo_bits != 8)
     return set_error(MIKV_ERR_UNSUPPORTED, "lo_bits must be 0, 2, 3, 4 or 8 (got %d)", c->lo_bits);
-  if (c->lo_bits == 3 && G > 2)
-    return set_error(MIKV_ERR_UNSUPPORTED, "a 3-bit retained pool serves at most 2 query heads per KV head (got %d)", G);
   if (c->cap_hi < 1 || (!evicting(c) && c->cap_lo < 1) || c->max_len < 1)
     return set_error(MIKV_ERR_INVALID_ARG, "cap_hi, cap_lo (unless lo_bits is 0) and max_len must be >= 1");
   if (int2_values_tiled(c->lo_bits, c->q_heads, c->kv_heads) && c->cap_lo % 32 != 0)

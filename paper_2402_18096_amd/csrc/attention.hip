@@ -125,13 +125,14 @@ struct Fmt {
       for (int j = 0; j < CPL / 2; ++j) out[j] = raw[j];
     } else if constexpr (BITS == 3) {
       // 3-bit codes straddle bytes and words: each pair (channels 2j,
-      // 2j+1, bits 6j .. 6j+5 of the lane's 96) is extracted from the
-      // 64-bit window that holds it into the low bits of the two halves
-      static_assert(CPL == 32, "3-bit rows: 32 channels per lane");
+      // 2j+1, bits 6j .. 6j+5 of the lane's 3 CPL bits, which start at bit
+      // 0 of raw[0]) is extracted from the 64-bit window that holds it into
+      // the low bits of the two halves
+      constexpr int KW = CPL == 32 ? 3 : 2;
 #pragma unroll
       for (int j = 0; j < CPL / 2; ++j) {
         const int bit = 6 * j, wi = bit / 32, sh = bit % 32;
-        const uint64_t win = ((uint64_t)(wi + 1 < 3 ? raw[wi + 1] : 0u) << 32) | raw[wi];
+        const uint64_t win = ((uint64_t)(wi + 1 < KW ? raw[wi + 1] : 0u) << 32) | raw[wi];
         const uint32_t x = (uint32_t)(win >> sh);
         out[j] = (x & 7u) | (((x >> 3) & 7u) << 16);
       }
@@ -166,6 +167,24 @@ struct Fmt {
 
 __device__ inline half2_t as_h2(uint32_t u) { return __builtin_bit_cast(half2_t, u); }
 
+// Codes enter the dot products as fp16 subnormals code * 2^(cls - 24), so
+// the query channel paired with a code of class cls is scaled by 2^-cls.
+// Scaled down, a small query channel would itself become an fp16 subnormal
+// and lose bits (and the matrix cores handle subnormal operands at reduced
+// precision), so the query is instead scaled by 2^(shift - cls) with shift
+// = the format's largest cls: never below 1, exact in fp16.  A wave whose
+// largest |q_hat| would overflow fp16 that way keeps shift 0.  The shift is
+// undone in the score scale (wave-uniform).
+template <int MAXCLS>
+__device__ inline int query_shift(float qmax_lane) {
+  if constexpr (MAXCLS == 0) {
+    return 0;
+  } else {
+    const float m = wave_max(qmax_lane);
+    return m * (float)(1 << MAXCLS) < 60000.0f ? MAXCLS : 0;
+  }
+}
+
 // Sum over the LPT consecutive lanes of a token (LPT = 4 or 8).
 template <int LPT>
 __device__ inline float token_sum(float v) {
@@ -191,9 +210,12 @@ __device__ inline float sum_token_lanes(float v) {
   return v;
 }
 
+// A 3-bit lane segment of 16 channels is 48 bits: two dwords are loaded
+// from the dword that holds its first bit and shifted (seg_shift) so that
+// the segment starts at bit 0.
 template <int BITS, int CPL>
 struct Rows {
-  static constexpr int KW = BITS == 16 ? CPL / 2 : CPL * BITS / 32;  // raw dwords per row segment
+  static constexpr int KW = BITS == 16 ? CPL / 2 : BITS == 3 && CPL == 16 ? 2 : CPL * BITS / 32;  // raw dwords per segment
   uint32_t k[KW], v[KW];
   uint32_t kp, vp;
 };
@@ -288,12 +310,11 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   const uint32_t *vpb = Q ? (is_hi ? A.hi_vp : A.lo_vp) + (int64_t)h * cap * ng : nullptr;
   float *scores = is_hi ? A.scores_hi : A.scores_lo;
   const float s2scale = A.scale * kLog2e;
-  const float s2scale_q = Q ? __builtin_ldexpf(s2scale, 24) : s2scale;
 
   // Query (Eq. 4: q / balance), as fp16 pairs matching the format's pairing,
-  // each pair pre-scaled by 2^-cls; with SPLITQ a second fp16 pair carries
-  // the rounding remainder.  qsum24 = 2^-24 * the sum of the lane's query
-  // channels (fp32).
+  // each pair scaled by 2^(qshift - cls) (query_shift); with SPLITQ a second
+  // fp16 pair carries the rounding remainder.  qsum24 = 2^(qshift - 24) * the
+  // sum of the lane's query channels (fp32).
   float m2[G], l[G], bsum[G], o[G][CPL];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
@@ -308,7 +329,21 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   // chunks are whole multiples of 128 tokens, at most max_chunk(G): an
   // iteration never runs past the LDS score buffer
   static_assert(128 % kPerIter == 0 && max_chunk(G) % 128 == 0, "iteration must divide 128 tokens");
-  constexpr int kSeg = Rows<BITS, CPL>::KW * 4;  // bytes of one lane's row segment
+  constexpr int kSeg = Rows<BITS, CPL>::KW * 4;  // bytes loaded per lane's row segment
+  // byte offset of the lane's segment in a row, and the bit shift that
+  // aligns it (non-zero only for the 48-bit 3-bit segments of odd lanes)
+  constexpr bool kSeg48 = BITS == 3 && CPL == 16;
+  const uint32_t seg_off = kSeg48 ? 4u * (uint32_t)((3 * part) / 2) : (uint32_t)(part * kSeg);
+  const int seg_shift = kSeg48 && (part & 1) ? 16 : 0;
+  auto seg_words = [&](const uint32_t *raw, uint32_t *out) {
+    if constexpr (kSeg48) {
+      out[0] = seg_shift ? __builtin_amdgcn_alignbit(raw[1], raw[0], 16) : raw[0];
+      out[1] = seg_shift ? raw[1] >> 16 : raw[1];
+    } else {
+#pragma unroll
+      for (int i = 0; i < Rows<BITS, CPL>::KW; ++i) out[i] = raw[i];
+    }
+  };
   const int n_iter = end > start ? (end - start + kPerIter - 1) / kPerIter : 0;
   const int first = start + wave * TPW * UNROLL + tsub;  // this lane's token in iteration 0, u = 0
   const int g_lane = (part * CPL) / A.group;
@@ -320,7 +355,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
                          : make_rsrc(Q ? (const void *)kpb : (const void *)kb, Q ? (uint32_t)n_pool * ng * 4u : 0u);
   const rsrc_t rvp = make_rsrc(Q ? (const void *)vpb : (const void *)vb, Q ? (uint32_t)n_pool * ng * 4u : 0u);
   const uint32_t lane_tok = (uint32_t)(start + wave * TPW * UNROLL + tsub);
-  const uint32_t off_row0 = lane_tok * (uint32_t)kRow + (uint32_t)(part * kSeg);
+  const uint32_t off_row0 = lane_tok * (uint32_t)kRow + seg_off;
   const uint32_t off_par0 = (lane_tok * (uint32_t)ng + (uint32_t)g_lane) * 4u;
   const uint32_t off_kp0 = KPC ? lane_tok * 4u : off_par0;
 
@@ -377,6 +412,29 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
       bal[4 * j + 3] = v.w;
     }
   }
+  constexpr int kMaxCls = BITS == 2 ? 6 : BITS == 4 ? 4 : 0;
+  int qshift = 0;
+  if constexpr (kMaxCls > 0 && !KPC) {
+    // bound on |q_hat| over the wave: max |q| / min b
+    uint32_t mb = 0;
+#pragma unroll
+    for (int i = 0; i < G; ++i)
+#pragma unroll
+      for (int j = 0; j < CPL / 8; ++j) {
+        const uint32_t w[4] = {qraw[i][j].x, qraw[i][j].y, qraw[i][j].z, qraw[i][j].w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) mb = max(mb, max(w[k] & 0x7fffu, (w[k] >> 16) & 0x7fffu));
+      }
+    float bound = f16_to_f32((uint16_t)mb);
+    if constexpr (SPLITQ) {
+      float bmin = bal[0];
+#pragma unroll
+      for (int c = 1; c < CPL; ++c) bmin = fminf(bmin, bal[c]);
+      bound = bound / bmin;
+    }
+    qshift = query_shift<kMaxCls>(bound);
+  }
+  const float s2scale_q = Q ? __builtin_ldexpf(s2scale, 24 - qshift) : s2scale;
 #pragma unroll
   for (int i = 0; i < G; ++i) {
     float qf[CPL];
@@ -401,10 +459,10 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
     float s = 0.0f;
 #pragma unroll
     for (int c = 0; c < CPL; ++c) s += qhat(c);
-    qsum24[i] = __builtin_ldexpf(s, -24);
+    qsum24[i] = __builtin_ldexpf(s, qshift - 24);
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
-      const float sc = __builtin_ldexpf(1.0f, -F::cls(p));
+      const float sc = __builtin_ldexpf(1.0f, qshift - F::cls(p));
       const float a = qhat(F::lo(p)) * sc, bb = qhat(F::hi(p)) * sc;
       const _Float16 ah = (_Float16)a, bh = (_Float16)bb;
       qh[i][p] = half2_t{ah, bh};
@@ -464,8 +522,9 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       valid[u] = first < rem - u * TPW;
-      uint32_t kx[NP];
-      F::template unpack<CPL>(cur[u].k, kx);
+      uint32_t kx[NP], kraw[Rows<BITS, CPL>::KW];
+      seg_words(cur[u].k, kraw);
+      F::template unpack<CPL>(kraw, kx);
       const half2_t kab = as_h2(cur[u].kp);  // (alpha, beta) of the key group
       if constexpr (KPC) {
         // the token's key block (the parameter word is its position); tokens
@@ -529,8 +588,9 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   auto proc_v = [&](Rows<BITS, CPL>(&cur)[UNROLL]) {
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
-      uint32_t vx[NP];
-      F::template unpack<CPL>(cur[u].v, vx);
+      uint32_t vx[NP], vraw[Rows<BITS, CPL>::KW];
+      seg_words(cur[u].v, vraw);
+      F::template unpack<CPL>(vraw, vx);
       const half2_t vab = as_h2(cur[u].vp);  // (alpha, beta) of the value group
 #pragma unroll
       for (int i = 0; i < G; ++i) {
@@ -643,10 +703,15 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 // The 2-bit retained pool on the matrix cores (16x16x32 fp16 MFMA).
 //
 // Lane l = 16 a + n.  Scores of a 16-token tile: B holds the tile's key
-// codes as exact fp16 subnormals (code * 2^(2k-24), k the code's position
-// class); lane (n, a) holds the 32 codes of channels [32a, 32a + 32) of
-// token n, so the token-major key rows are read as they are stored.  A
-// holds the query: row 4 s + gamma carries q_hat (times 2^-2k) of query
+// codes as exact fp16 subnormals: the 2-bit field of class k (its position
+// in the byte) is shifted to mantissa bits 6-7 (k even: code * 2^-18) or
+// 8-9 (k odd: code * 2^-16) of its 16-bit half.  The matrix cores multiply
+// the deepest fp16 subnormals (code * 2^-24, 2^-22) at reduced precision,
+// about 5e-6 relative, but subnormals from 2^-18 up exactly (measured).
+// Lane (n, a) holds the 32 codes of channels [32a, 32a + 32) of token n, so
+// the token-major key rows are read as they are stored.  A
+// holds the query: row 4 s + gamma carries q_hat (times 2^qshift, and 4 more
+// for even classes, so every product is q * code * 2^(qshift - 16)) of query
 // slot s on the channels of quantization group gamma and 0 elsewhere, so
 // lane (n, a) receives, for query slot a, one partial dot product per group
 // and applies token n's per-group scale and zero (folded Eq. 1).
@@ -654,8 +719,9 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 // Value sums: the pool's value codes are stored in 32-slot tiles,
 // quad-major (int2_v_byte).  For n-block nb (channels 16nb..16nb+15) lane
 // (n, g) reads the 8 bytes of quad 4nb + n/4 for slots 8g..8g+7 and keeps
-// field n%4: B = codes (tokens x channels, column scale 2^(2(n%4)-24), undone
-// on the output); A = the softmax weights e * alpha of the column's group,
+// field n%4, shifted as the key fields: B = codes (tokens x channels, column
+// scale 2^-18 or 2^-16, undone on the output); A = the softmax weights
+// e * alpha of the column's group,
 // split in an fp16 high and low part (rows 2i and 2i+1 for query i) and
 // staged through LDS into the operand layout.
 // ---------------------------------------------------------------------------
@@ -719,7 +785,6 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   const int end = min(start + A.chunk_lo, n_pool);
   const int n_iter = end > start ? (end - start + kItTok - 1) / kItTok : 0;
   float *scores = A.scores_lo;
-  const float s2scale_q = __builtin_ldexpf(A.scale * kLog2e, 24);
 
   const rsrc_t rk = make_rsrc(A.lo_k + (int64_t)h * cap * 32, (uint32_t)n_pool * 32u);
   const rsrc_t rv = make_rsrc(A.lo_v + (int64_t)h * cap * 32, (uint32_t)((n_pool + 31) / 32) * 1024u);
@@ -797,6 +862,9 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   // QS) of set st, group m%4, over K block a (channels [32a, 32a + 32)).
   h8_t AK[NSET][NP][4];
   float qpart[NSET];
+  // the query scaled by 2^(qshift - 2 k) for class k (query_shift)
+  float qfs[NSET][32];
+  float qmax = 0.0f;
 #pragma unroll
   for (int st = 0; st < NSET; ++st) {
     const int iq = (n / 4) % QS + 4 * st;
@@ -804,7 +872,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
     uint4 qr[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) qr[j] = q4[j];
-    float qf[32];
+    float *qf = qfs[st];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const uint32_t w[4] = {qr[j].x, qr[j].y, qr[j].z, qr[j].w};
@@ -825,6 +893,17 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         qf[4 * j + 3] = qf[4 * j + 3] / v.w;
       }
     }
+#pragma unroll
+    for (int j = 0; j < 32; ++j) qmax = fmaxf(qmax, fabsf(qf[j]));
+  }
+  // the even-class query operand carries 2^(qshift + 2): largest qshift in
+  // {6, 4, 2, 0} that keeps it within fp16 (wave-uniform)
+  const float qm = wave_max(qmax);
+  const int qshift = qm * 256.0f < 60000.0f ? 6 : qm * 64.0f < 60000.0f ? 4 : qm * 16.0f < 60000.0f ? 2 : 0;
+  const float s2scale_q = __builtin_ldexpf(A.scale * kLog2e, 16 - qshift);
+#pragma unroll
+  for (int st = 0; st < NSET; ++st) {
+    const float *qf = qfs[st];
     float ps = 0.0f;
 #pragma unroll
     for (int j = 0; j < 32; ++j) ps += qf[j];
@@ -840,7 +919,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         for (int hf = 0; hf < 2; ++hf) {
           const int e = 2 * d + hf;
           const int j = 16 * (i >> 1) + 4 * (i & 1) + (e >> 1) + 8 * (e & 1);
-          vv[hf] = qf[j] * (keep * __builtin_ldexpf(1.0f, -2 * (e >> 1)));
+          vv[hf] = qf[j] * (keep * __builtin_ldexpf(1.0f, qshift + ((e >> 1) & 1 ? 0 : 2)));
         }
         const _Float16 h0 = (_Float16)vv[0], h1 = (_Float16)vv[1];
         hw[d] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
@@ -871,7 +950,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       float v = all[0][gm];
 #pragma unroll
       for (int s3 = 1; s3 < QS; ++s3) v = qs == s3 ? all[s3][gm] : v;
-      qsl[st][gm] = __builtin_ldexpf(v, -24);  // 2^-24: the scale of the scores below
+      qsl[st][gm] = __builtin_ldexpf(v, qshift - 16);  // 2^(qshift - 16): the scale of the scores below
     }
   }
 
@@ -895,7 +974,11 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   f4_t CV[8];
 #pragma unroll
   for (int nb = 0; nb < 8; ++nb) CV[nb] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
-  const uint32_t mk = 0x00030003u << (2 * (n & 3));  // value field of this lane's column
+  // value field n % 4 of this lane's column, moved like the key fields: from
+  // bytes 0, 2 left by vsl, from bytes 1, 3 right by vsr, to bits vpos
+  const int vpos = (n & 1) ? 8 : 6;
+  const int vsl = vpos - 2 * (n & 3), vsr = 8 + 2 * (n & 3) - vpos;
+  const uint32_t mk = 0x00030003u << vpos;
 
   // Half-step pipeline (as in attn_chunk): the next iteration's keys are
   // loaded once the scores are done, its values once the value MFMAs are.
@@ -907,15 +990,22 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
     uint64_t raise = 0;
 #pragma unroll
     for (int q = 0; q < kKT; ++q) {
+      // code pairs of bytes 0, 2 (fields k at bits 2k) and bytes 1, 3
+      // (bits 8 + 2k), each field moved to bits 6-7 (k even) or 8-9 (k odd)
+      // of its half: code * 2^-18 or code * 2^-16
       uint32_t P[16];
 #pragma unroll
       for (int w = 0; w < 2; ++w) {
-        const uint32_t x = cur.kc[q][w], y = x >> 8;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          P[(2 * w) * 4 + k] = x & (0x00030003u << (2 * k));
-          P[(2 * w + 1) * 4 + k] = y & (0x00030003u << (2 * k));
-        }
+        const uint32_t x = cur.kc[q][w];
+        const uint32_t l6 = x << 6, l2 = x << 2, r2 = x >> 2, r6 = x >> 6;
+        P[(2 * w) * 4 + 0] = l6 & 0x00c000c0u;
+        P[(2 * w) * 4 + 1] = l6 & 0x03000300u;
+        P[(2 * w) * 4 + 2] = l2 & 0x00c000c0u;
+        P[(2 * w) * 4 + 3] = l2 & 0x03000300u;
+        P[(2 * w + 1) * 4 + 0] = r2 & 0x00c000c0u;
+        P[(2 * w + 1) * 4 + 1] = r2 & 0x03000300u;
+        P[(2 * w + 1) * 4 + 2] = r6 & 0x00c000c0u;
+        P[(2 * w + 1) * 4 + 3] = r6 & 0x03000300u;
       }
       const bool valid = t0 + 16 * q + n < end;
 #pragma unroll
@@ -926,7 +1016,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #pragma unroll
           for (int i = 0; i < 4; ++i)
             C = mfma32(AK[st][pt][i], pack_h8(P[4 * i], P[4 * i + 1], P[4 * i + 2], P[4 * i + 3]), C);
-        // 2^-24 times the folded score (the fp16 scale and zero enter
+        // 2^(qshift - 16) times the folded score (the fp16 scale and zero enter
         // mixed-precision FMAs as stored; the power of two is in the scale)
         float s = 0.0f;
 #pragma unroll
@@ -1027,7 +1117,8 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
         const uint32_t d0 = cur.vc[vt][nb][0], d1 = cur.vc[vt][nb][1];
-        CV[nb] = mfma32(AV[(16 * nb) / GROUP], pack_h8(d0 & mk, (d0 >> 8) & mk, d1 & mk, (d1 >> 8) & mk), CV[nb]);
+        CV[nb] = mfma32(AV[(16 * nb) / GROUP],
+                        pack_h8((d0 << vsl) & mk, (d0 >> vsr) & mk, (d1 << vsl) & mk, (d1 >> vsr) & mk), CV[nb]);
       }
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -1065,7 +1156,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   }
   // Record per query: max, normaliser, value sums (lane group i/2 holds
   // query i in registers 2(i%2), 2(i%2)+1).
-  const float colscale = __builtin_ldexpf(1.0f, 24 - 2 * (n & 3));
+  const float colscale = __builtin_ldexpf(1.0f, 24 - vpos);
 #pragma unroll
   for (int i = 0; i < G; ++i) {
     float *rec = A.partials + ((int64_t)(qh0 + i) * nc + rec_chunk) * kRec;
@@ -1191,9 +1282,6 @@ void attn_partial_kernel(AttnArgs A) {
       attn_chunk_int2<G, SPLITQ, 2>(A, h, c - A.nc_hi, c, s_lds, w_lds);
     else
       attn_chunk_int2<G, SPLITQ, 1>(A, h, c - A.nc_hi, c, s_lds, w_lds);
-  } else if constexpr (LO == 3 && CPL != 32) {
-    // not reached: the host rejects 3-bit retained pools above two query
-    // heads per KV head
   } else {
     attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
   }

@@ -58,8 +58,22 @@ def test_cache_validation_errors(field, value, code):
     assert mikv.lib().mikv_last_error()
 
 
-def test_three_bit_retained_pool_at_most_two_query_heads_per_kv_head():
-    assert _call_attention(_desc(lo_bits=3, q_heads=4, kv_heads=1)) == 2
+def test_per_channel_keys_supported_formats():
+    """Per-channel key blocks (Appendix C): 64 positions, fp16 importance pool,
+    2/3/4-bit retained codes, one query head per KV head, block parameters
+    given; anything else is refused before a launch."""
+    assert _call_attention(_desc(key_block=32, lo_kb=0x1000)) == 2
+    assert _call_attention(_desc(key_block=64, lo_kb=0x1000, q_heads=4, kv_heads=2)) == 2
+    assert _call_attention(_desc(key_block=64, lo_kb=0x1000, hi_bits=8, hi_kp=0x1000, hi_vp=0x1000)) == 2
+    assert _call_attention(_desc(key_block=64, lo_kb=0x1000, lo_bits=8)) == 2
+    assert _call_attention(_desc(key_block=64)) == 1                     # lo_kb missing
+    L = mikv.lib()
+    p = ctypes.c_void_p(0x1000)
+    c = _desc(key_block=64, lo_kb=0x1000, max_len=256, cap_lo=256)
+    # the re-rank and the decode step need a window of at least one key block
+    assert L.mikv_select_topk(ctypes.byref(c), 4, 1, 32, None, p, 1 << 20, None) == 1
+    assert L.mikv_decode_step(ctypes.byref(c), 4, p, p, p, None, 0.1, p, p, None, 1, 32, 0, p, 1 << 30, None,
+                              None) == 1
 
 
 def test_int4_importance_pool_needs_two_bit_or_evicting_retained_pool():

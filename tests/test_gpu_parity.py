@@ -156,6 +156,63 @@ def test_full_size_sampled_heads(name):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("name", ["mistral_7b", "long_context"])
+def test_full_size_whole_trajectory(name):
+    """The GQA and long-context workloads at full size through their whole
+    step count (128 and 256 decode steps) in the benchmark's launch
+    configuration: attention output and probabilities of three sampled heads
+    checked every step, the bit-exact state every 16th step and at the end."""
+    _dev()
+    wl = workloads.WORKLOADS[name]
+    NH = wl.n_heads
+    print(f"[trajectory] {name}: {NH} heads, context {wl.context}, {wl.steps} steps", flush=True)
+    run = SampledLockstep(wl, wl.steps, heads=[0, NH // 2 + 1, NH - 1])
+    run.prefill()
+    worst = 0.0
+    for t in range(wl.steps):
+        worst = max(worst, run.step(t, check_state=t % 16 == 15 or t == wl.steps - 1))
+    print(f"[trajectory] {name}: max |o - o_ref| over {wl.steps} steps {worst:.3e}", flush=True)
+    del run
+    torch.cuda.empty_cache()
+
+
+def test_free_running_trajectory_report():
+    """The oracle free-running beside the GPU (each ranks with its own
+    probabilities) on the long_context workload for 32 steps: a report of
+    precision-map differences and near-ties at the cut (not a gate), and,
+    while the maps still agree, attention outputs within tolerance."""
+    _dev()
+    import json
+
+    from tests.parity import O_ATOL
+    from tests.trajectory import run_report
+    wl = workloads.WORKLOADS["long_context"]
+    rep = run_report(wl, 32, [0, wl.n_heads // 2 + 1, wl.n_heads - 1])
+    summary = {k: v for k, v in rep.items() if k != "per_step"}
+    print("[trajectory report] " + json.dumps(summary), flush=True)
+    assert len(rep["per_step"]) == 32
+    assert rep["max_abs_o_diff_before_divergence"] is None or rep["max_abs_o_diff_before_divergence"] < 2 * O_ATOL
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("scale", [20.0, 40.0])
+def test_lockstep_gqa_outlier_margin(scale):
+    """The Mistral shape with its 8 outlier channels at x20 and x40: the
+    attention output must stay within a quarter of the allowed error (the
+    matrix-core loop multiplies no code below 2^-18, where the matrix cores
+    lose precision), every step bit-exact otherwise."""
+    _dev()
+    wl = workloads.small_workload("mistral_7b", batch=1, q_heads=8, kv_heads=2, context=16384, kv_outlier_scale=scale)
+    run = Lockstep(wl, 6, fused=True)
+    run.prefill()
+    worst = 0.0
+    for t in range(6):
+        run.step(t)
+        worst = max(worst, run.last_margin)
+    print(f"[outlier x{scale:g}] largest share of the output allowance used: {worst:.3f}", flush=True)
+    assert worst < 0.25
+
+
 def test_lockstep_gqa8():
     """Eight query heads per KV head (Llama-2-70b's grouping)."""
     _dev()
@@ -338,6 +395,8 @@ def test_full_size_int4_importance_sampled_heads():
     ("llama2_7b", {}),                                    # INT8 importance pool, group 64
     ("llama2_13b", {}),                                   # balanced INT8 importance pool
     ("mistral_7b", dict(q_heads=4, kv_heads=2)),          # two query heads per KV head
+    ("mistral_7b", {}),                                   # four (16-channel lanes, 48-bit code segments)
+    ("mistral_7b", dict(batch=1, q_heads=16, kv_heads=2, context=900)),  # eight
 ])
 @pytest.mark.parametrize("fused", [False, True])
 def test_lockstep_int3_retained_cache(name, extra, fused):
@@ -351,13 +410,15 @@ def test_lockstep_int3_retained_cache(name, extra, fused):
         run.step(t)
 
 
-def test_full_size_int3_retained_sampled_heads():
-    """The INT3 retained cache at the long_context size in the benchmark's
-    launch configuration, the oracle following three heads."""
+@pytest.mark.parametrize("name", ["long_context", "mistral_7b"])
+def test_full_size_int3_retained_sampled_heads(name):
+    """The INT3 retained cache at the long_context and Mistral (GQA, four
+    query heads per KV head) sizes in the benchmark's launch configuration,
+    the oracle following three heads."""
     _dev()
-    wl = workloads.WORKLOADS["long_context"].with_(lo_bits=3)
+    wl = workloads.WORKLOADS[name].with_(lo_bits=3)
     NH = wl.n_heads
-    print(f"[full-size int3 retained] long_context: {NH} heads, 2 steps", flush=True)
+    print(f"[full-size int3 retained] {name}: {NH} heads, 2 steps", flush=True)
     run = SampledLockstep(wl, 2, heads=[0, NH // 2 + 1, NH - 1])
     run.prefill()
     for t in range(2):
