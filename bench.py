@@ -408,7 +408,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--workload", default="long_context")
     ap.add_argument("--secondary", default="llama2_13b",
-                    help="a second workload timed in the same run and reported under `secondary` ('' for none); "
+                    help="a second workload timed in the same run and reported under `secondary` ('none' for none); "
                          "it runs min(--steps, its own step count) timed steps")
     ap.add_argument("--fused", type=int, default=1, help="fuse the importance update into attention (default 1)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
@@ -449,7 +449,7 @@ def main():
     cpu_s = 0.0 if args.no_cpu_baseline else args.cpu_seconds
     head = run_workload(wl, args, args.steps, args.warmup, cpu_s, bool(args.override))
     secondary = None
-    if args.secondary and args.secondary != args.workload:
+    if args.secondary and args.secondary not in ("none", args.workload):
         wl2 = apply_overrides(workloads.WORKLOADS[args.secondary], args.override)
         secondary = run_workload(wl2, args, min(args.steps, wl2.steps), args.warmup, cpu_s * 2 / 3,
                                  bool(args.override))
