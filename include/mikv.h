@@ -94,6 +94,12 @@ enum mikv_attention_flags {
  *   probs_lo is not written, and map 0 means "evicted".
  * Codes: Eq. 1 per token and per group of `group` contiguous channels, packed
  * least-significant-bits first (channel c at byte c*N/8, bit (c*N)%8).
+ * Exception: 2-bit retained values of a cache shared by two or more query
+ *   heads (q_heads >= 2 * kv_heads) are stored in tiles of 32 slots (cap_lo a
+ *   multiple of 32) for the matrix cores: byte q (0..31) of slot s holds
+ *   channels q, q+32, q+64, q+96 at bits 0-1, 2-3, 4-5, 6-7 and sits at
+ *   (s/32)*1024 + 16*(16*((s%32)/8) + q%16) + 8*(q/16) + s%8 of the head's
+ *   array (same size as the token-major one).
  * Keys are stored balanced (Eq. 3) when a balancer is in use.
  * map [NH, max_len] uint8 (nullable): 1 = position in the importance pool,
  *   0 = retained pool; maintained by mikv_quantize_kv and mikv_select_topk.

@@ -33,6 +33,7 @@
 // scores; the finalize phase merges the records exactly, turns scores into
 // probabilities and optionally adds them to the importance scores.
 #include <algorithm>
+#include <numeric>
 #include <type_traits>
 
 #include "append_device.h"
@@ -716,11 +717,12 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
 // lane (n, a) receives, for query slot a, one partial dot product per group
 // and applies token n's per-group scale and zero (folded Eq. 1).
 //
-// Value sums: the pool's value codes are stored in 32-slot tiles,
-// quad-major (int2_v_byte).  For n-block nb (channels 16nb..16nb+15) lane
-// (n, g) reads the 8 bytes of quad 4nb + n/4 for slots 8g..8g+7 and keeps
-// field n%4, shifted as the key fields: B = codes (tokens x channels, column
-// scale 2^-18 or 2^-16, undone on the output); A = the softmax weights
+// Value sums: the pool's value codes are stored in 32-slot tiles
+// (int2_v_byte): lane (n, g) reads, in one 16-byte load, bytes n and n + 16
+// of slots 8g..8g+7, whose fields are channels n + 32j and n + 16 + 32j.
+// For n-block nb (channels 16nb..16nb+15) it takes field nb/2 of byte
+// n + 16(nb%2), moved to bits 8-9 of its half: B = codes * 2^-16 (tokens x
+// channels, the scale undone on the output); A = the softmax weights
 // e * alpha of the column's group,
 // split in an fp16 high and low part (rows 2i and 2i+1 for query i) and
 // staged through LDS into the operand layout.
@@ -756,6 +758,12 @@ __device__ inline float row_sum16(float v) {
 constexpr int kKT = MIKV_INT2_KEY_TILES;  // 16-token key tiles per iteration (2 or 4)
 constexpr int kVT = kKT / 2;              // 32-token value tiles per iteration
 constexpr int kItTok = 16 * kKT;          // tokens per iteration
+// Iterations whose loads are in flight at once (register buffers): three
+// while the registers allow it, one with eight query heads per KV head.
+#ifndef MIKV_INT2_DEPTH
+#define MIKV_INT2_DEPTH 1
+#endif
+__host__ __device__ constexpr int int2_depth(int G) { return G <= 4 ? MIKV_INT2_DEPTH : 1; }
 // Operand element -> slot inside a lane group's 8 (and back): bits 0 and 1
 // swapped, the order the masked code pairs come out in.
 __host__ __device__ constexpr int tau8(int e) { return (e & 4) | ((e & 1) << 1) | ((e >> 1) & 1); }
@@ -797,7 +805,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
     uint32_t kc[kKT][2];
     uint32_t kp[kKT][NG];
     uint32_t vp[kKT][NGL];
-    uint32_t vc[kVT][8][2];
+    uint32_t vc[kVT][4];
   };
   // KEYS: the key codes and parameters; VALS: the value codes and
   // parameters.  With `live` false every load goes through an empty
@@ -827,26 +835,36 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         }
       }
       if (vals) {
+        if constexpr (R == 1 && NG == 4) {  // every group: the whole row, one load
+          auto vp = __builtin_amdgcn_raw_buffer_load_b128(avp, slot * 16u, 0, 0);
 #pragma unroll
-        for (int j = 0; j < NGL; ++j)
-          d.vp[q][j] = __builtin_amdgcn_raw_buffer_load_b32(avp, (slot * NG + (uint32_t)((rho + R * j) % NG)) * 4u, 0, 0);
+          for (int j = 0; j < 4; ++j) d.vp[q][j] = vp[j];
+        } else if constexpr (R == 1 && NG == 2) {
+          auto vp = __builtin_amdgcn_raw_buffer_load_b64(avp, slot * 8u, 0, 0);
+          d.vp[q][0] = vp[0];
+          d.vp[q][1] = vp[1];
+        } else {
+#pragma unroll
+          for (int j = 0; j < NGL; ++j)
+            d.vp[q][j] = __builtin_amdgcn_raw_buffer_load_b32(avp, (slot * NG + (uint32_t)((rho + R * j) % NG)) * 4u, 0, 0);
+        }
       }
     }
     if (vals) {
 #pragma unroll
       for (int vt = 0; vt < kVT; ++vt) {
         const uint32_t tile = (t0 >> 5) + vt;
+        auto vc = __builtin_amdgcn_raw_buffer_load_b128(av, tile * 1024u + 16u * (uint32_t)lane, 0, 0);
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) {
-          auto vc = __builtin_amdgcn_raw_buffer_load_b64(av, tile * 1024u + (uint32_t)(4 * nb + n / 4) * 32u + 8u * a, 0, 0);
-          d.vc[vt][nb][0] = vc[0];
-          d.vc[vt][nb][1] = vc[1];
-        }
+        for (int j = 0; j < 4; ++j) d.vc[vt][j] = vc[j];
       }
     }
   };
-  Ld cur;
-  if (n_iter > 0) load(cur, 0, true, true, true);
+  // kDepth iterations in flight: buffer d holds iterations d, d + kDepth, ...
+  constexpr int kDepth = int2_depth(G);
+  Ld buf[kDepth];
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d) load(buf[d], d, true, true, d < n_iter);
 
   // zero the weight rows (rows past 2G are never written)
   {
@@ -974,16 +992,14 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   f4_t CV[8];
 #pragma unroll
   for (int nb = 0; nb < 8; ++nb) CV[nb] = f4_t{0.0f, 0.0f, 0.0f, 0.0f};
-  // value field n % 4 of this lane's column, moved like the key fields: from
-  // bytes 0, 2 left by vsl, from bytes 1, 3 right by vsr, to bits vpos
-  const int vpos = (n & 1) ? 8 : 6;
-  const int vsl = vpos - 2 * (n & 3), vsr = 8 + 2 * (n & 3) - vpos;
-  const uint32_t mk = 0x00030003u << vpos;
+  // value fields go to bits 8-9 of each half (code * 2^-16)
+  constexpr uint32_t mk = 0x03000300u;
 
-  // Half-step pipeline (as in attn_chunk): the next iteration's keys are
-  // loaded once the scores are done, its values once the value MFMAs are.
-  for (int it = 0; it < n_iter; ++it) {
-    const bool live = it + 1 < n_iter;
+  // Iteration `it` from buffer `cur`, which is then refilled with iteration
+  // it + kDepth: its keys once the scores are done, its values once the
+  // value MFMAs are.
+  auto body = [&](Ld &cur, int it) {
+    const bool live = it + kDepth < n_iter;
     const int t0 = start + it * kItTok;
     // --- scores of the four key tiles
     float s2[kKT][NSET];
@@ -1026,7 +1042,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         }
         const float v2 = valid ? s * s2scale_q : kNegInf;
         s2[q][st] = v2;
-        if (scores) s_lds[(qs + 4 * st) * max_chunk(G) + (t0 - start) + 16 * q + n] = v2;  // replicas agree
+        if (scores && t0 < end) s_lds[(qs + 4 * st) * max_chunk(G) + (t0 - start) + 16 * q + n] = v2;  // replicas agree
         raise |= __ballot(v2 > m_own[st] + kLazy);
       }
     }
@@ -1081,7 +1097,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    load(cur, it + 1, true, false, live);
+    load(cur, it + kDepth, true, false, live);
     __builtin_amdgcn_sched_barrier(0);
     // --- weights e * alpha into LDS (the A layout of the value MFMAs)
 #pragma unroll
@@ -1116,17 +1132,31 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       for (int gm = 0; gm < NG; ++gm) AV[gm] = *reinterpret_cast<const h8_t *>(w_lds + w_index(gm, vt, n, a, 0));
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
-        const uint32_t d0 = cur.vc[vt][nb][0], d1 = cur.vc[vt][nb][1];
+        // channels 16 nb + n: segment j = nb / 2 (field j of every byte),
+        // bytes n + 16 (nb % 2) of the lane's 8 slots
+        const int j = nb >> 1;
+        const uint32_t d0 = cur.vc[vt][2 * (nb & 1)], d1 = cur.vc[vt][2 * (nb & 1) + 1];
         CV[nb] = mfma32(AV[(16 * nb) / GROUP],
-                        pack_h8((d0 << vsl) & mk, (d0 >> vsr) & mk, (d1 << vsl) & mk, (d1 >> vsr) & mk), CV[nb]);
+                        pack_h8((d0 << (8 - 2 * j)) & mk, (d0 >> (2 * j)) & mk, (d1 << (8 - 2 * j)) & mk,
+                                (d1 >> (2 * j)) & mk),
+                        CV[nb]);
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    load(cur, it + 1, false, true, live);
+    load(cur, it + kDepth, false, true, live);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  // The bodies run unconditionally (a branch around one would make the
+  // compiler wait for every load in flight at the loop head): an iteration
+  // past the end reads through the empty descriptor and scores -inf, so it
+  // adds nothing.  Chunks of the pool are multiples of kDepth iterations
+  // (make_plan), so only a head's last chunk can run one.
+  for (int it = 0; it < n_iter; it += kDepth) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) body(buf[d], it + d);
   }
 
   // Scores of the chunk: one burst from LDS.
@@ -1156,7 +1186,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   }
   // Record per query: max, normaliser, value sums (lane group i/2 holds
   // query i in registers 2(i%2), 2(i%2)+1).
-  const float colscale = __builtin_ldexpf(1.0f, 24 - vpos);
+  constexpr float colscale = 65536.0f;  // undoes the value encoding (code * 2^-16)
 #pragma unroll
   for (int i = 0; i < G; ++i) {
     float *rec = A.partials + ((int64_t)(qh0 + i) * nc + rec_chunk) * kRec;
@@ -1615,7 +1645,13 @@ Plan make_plan(const mikv_cache *c, int length) {
   // long_context step); GQA rows carry G queries' work and keep one share
   const int64_t target_hi = group_size_of(c) == 1 ? target * MIKV_CHUNK_HI_SCALE : target;
   p.chunk_hi = std::min(cmax, std::max(128, round_up(target_hi / bh, 128)));
-  p.chunk_lo = std::min(cmax, std::max(128, round_up(target / bl, 128)));
+  // the 2-bit pool under GQA runs on the matrix cores, int2_depth(G)
+  // iterations of kItTok tokens at a time: its chunks are whole multiples
+  // of that too
+  const int G = group_size_of(c);
+  const bool mfma_lo = c->lo_bits == 2 && G >= 2 && c->key_block == 0;
+  const int mult_lo = mfma_lo ? std::lcm(128, kItTok * int2_depth(G)) : 128;
+  p.chunk_lo = std::min(cmax / mult_lo * mult_lo, std::max(mult_lo, round_up(target / bl, mult_lo)));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
   p.nc_lo = evicting(c) ? 0 : std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
   // every token is in one of the pools, so at least length - cap_hi are in

@@ -225,12 +225,15 @@ __device__ inline T *lane_pick(bool c, T *a, T *b) {
 }
 
 // ---------------------------------------------------------------------------
-// Retained-pool 2-bit value codes for GQA: tiles of 32 slots, quad-major.
-// A slot's LSB-first packed 2-bit row has 32 bytes; byte q holds channels
-// 4q..4q+3.  In a tiled value array that byte of slot s sits at (s / 32) * 1024 + 32 * q + (s % 32): the same channel quad
-// of 32 consecutive slots is contiguous, the operand shape the decode
-// attention's matrix cores read (tokens along the reduction).  Every byte
-// belongs to one slot, so slots are written independently.
+// Retained-pool 2-bit value codes for GQA: tiles of 32 slots.
+// Byte q (0..31) of a slot interleaves the four 32-channel segments: it
+// holds channels q, q + 32, q + 64 and q + 96 at bits 0-1, 2-3, 4-5 and 6-7.
+// In a tile (1024 bytes) byte q of slot s sits at
+//   16 * (16 * (s % 32 / 8) + q % 16) + 8 * (q / 16) + s % 8:
+// the 16 bytes at 16 l are bytes l % 16 and l % 16 + 16 of the 8 slots
+// 8 (l / 16) .. 8 (l / 16) + 7, which is what lane l of the decode
+// attention's value product uses (every field of every byte: one matrix-core
+// column block per segment, tokens along the reduction).
 // ---------------------------------------------------------------------------
 // The tiled value layout is used where the matrix cores read it: 2-bit
 // retained pools shared by two or more query heads (GQA).  With one query
@@ -240,15 +243,37 @@ __host__ __device__ inline bool int2_values_tiled(int lo_bits, int q_heads, int 
   return lo_bits == 2 && q_heads >= 2 * kv_heads;
 }
 
-__host__ __device__ inline int64_t int2_v_byte(int64_t slot, int quad) {
-  return (slot >> 5) * 1024 + (int64_t)quad * 32 + (slot & 31);
+__host__ __device__ inline int64_t int2_v_byte(int64_t slot, int q) {
+  return (slot >> 5) * 1024 + 16 * (16 * ((slot & 31) >> 3) + (q & 15)) + 8 * (q >> 4) + (slot & 7);
 }
 
-// Store the 8 packed bytes of channels [32 * part, 32 * part + 32) of a
-// slot's 2-bit value row (two little-endian words) into the tiled layout.
+// Store a slot's 2-bit value row into the tiled layout.  Called by the four
+// lanes of the row together (lanes 4k .. 4k+3 of the wave, segment `part` =
+// lane % 4, each with the 64 codes of its segment, channel 32 part + c at
+// bit 2c of w[0] | w[1] << 32): lane `part` gathers the 16-bit chunk `part`
+// of every segment's codes and writes bytes 8 part .. 8 part + 7.
 __device__ inline void store_int2_v(uint8_t *head_base, int64_t slot, int part, const uint32_t w[2]) {
+  uint32_t lo = 0u, hi = 0u;  // the lane's bytes 0-3 and 4-7
 #pragma unroll
-  for (int j = 0; j < 8; ++j) head_base[int2_v_byte(slot, 8 * part + j)] = (uint8_t)((w[j >> 2] >> (8 * (j & 3))) & 0xffu);
+  for (int r = 0; r < 4; ++r) {
+    // round r: this lane sends chunk part ^ r of its own segment and
+    // receives chunk `part` of segment part ^ r
+    const int want = part ^ r;
+    const uint32_t mine = (((want & 2) ? w[1] : w[0]) >> (16 * (want & 1))) & 0xffffu;
+    const uint32_t c = r == 0 ? mine : (uint32_t)__shfl_xor((int)mine, r, 64);
+    const int sh = 2 * (part ^ r);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t f = ((c >> (2 * e)) & 3u) << sh;
+      if (e < 4)
+        lo |= f << (8 * e);
+      else
+        hi |= f << (8 * (e - 4));
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    head_base[int2_v_byte(slot, 8 * part + e)] = (uint8_t)(((e < 4 ? lo : hi) >> (8 * (e & 3))) & 0xffu);
 }
 
 // ---------------------------------------------------------------------------

@@ -40,13 +40,19 @@ def np16(t: torch.Tensor) -> np.ndarray:
 
 
 def int2_values_token_major(v: np.ndarray, cap: int) -> np.ndarray:
-    """Retained-pool 2-bit value codes [NH, cap, 32] in the tiled layout
-    (byte (slot, quad) at slot//32 * 1024 + 32 * quad + slot % 32) back to
-    LSB-first token-major rows."""
+    """Retained-pool 2-bit value codes [NH, cap * 32] in the tiled layout back
+    to LSB-first token-major rows [NH, cap, 32].  Tiled: byte q of slot s (at
+    s//32 * 1024 + 16 * (16 * (s%32 // 8) + q % 16) + 8 * (q // 16) + s % 8)
+    holds channels q + 32 j at bits 2 j; token-major: channel c at bit 2 (c % 4)
+    of byte c // 4."""
     slot = np.arange(cap)[:, None]
-    quad = np.arange(32)[None, :]
-    idx = (slot // 32) * 1024 + 32 * quad + slot % 32
-    return v.reshape(v.shape[0], -1)[:, idx]
+    ch = np.arange(128)[None, :]
+    q, j = ch % 32, ch // 32
+    idx = (slot // 32) * 1024 + 16 * (16 * ((slot % 32) // 8) + q % 16) + 8 * (q // 16) + slot % 8
+    tiled = v.reshape(v.shape[0], -1)
+    codes = (tiled[:, idx] >> (2 * j)[None]) & 3                      # [NH, cap, 128]
+    c4 = codes.reshape(v.shape[0], cap, 32, 4).astype(np.uint8)
+    return (c4[..., 0] | (c4[..., 1] << 2) | (c4[..., 2] << 4) | (c4[..., 3] << 6)).astype(np.uint8)
 
 
 def gather_gpu_state(c: mikv.MikvCache, heads=None):
