@@ -33,7 +33,6 @@
 // scores; the finalize phase merges the records exactly, turns scores into
 // probabilities and optionally adds them to the importance scores.
 #include <algorithm>
-#include <numeric>
 #include <type_traits>
 
 #include "append_device.h"
@@ -758,12 +757,6 @@ __device__ inline float row_sum16(float v) {
 constexpr int kKT = MIKV_INT2_KEY_TILES;  // 16-token key tiles per iteration (2 or 4)
 constexpr int kVT = kKT / 2;              // 32-token value tiles per iteration
 constexpr int kItTok = 16 * kKT;          // tokens per iteration
-// Iterations whose loads are in flight at once (register buffers): three
-// while the registers allow it, one with eight query heads per KV head.
-#ifndef MIKV_INT2_DEPTH
-#define MIKV_INT2_DEPTH 1
-#endif
-__host__ __device__ constexpr int int2_depth(int G) { return G <= 4 ? MIKV_INT2_DEPTH : 1; }
 // Operand element -> slot inside a lane group's 8 (and back): bits 0 and 1
 // swapped, the order the masked code pairs come out in.
 __host__ __device__ constexpr int tau8(int e) { return (e & 4) | ((e & 1) << 1) | ((e >> 1) & 1); }
@@ -860,11 +853,8 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       }
     }
   };
-  // kDepth iterations in flight: buffer d holds iterations d, d + kDepth, ...
-  constexpr int kDepth = int2_depth(G);
-  Ld buf[kDepth];
-#pragma unroll
-  for (int d = 0; d < kDepth; ++d) load(buf[d], d, true, true, d < n_iter);
+  Ld cur;
+  load(cur, 0, true, true, n_iter > 0);
 
   // zero the weight rows (rows past 2G are never written)
   {
@@ -995,11 +985,10 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   // value fields go to bits 8-9 of each half (code * 2^-16)
   constexpr uint32_t mk = 0x03000300u;
 
-  // Iteration `it` from buffer `cur`, which is then refilled with iteration
-  // it + kDepth: its keys once the scores are done, its values once the
-  // value MFMAs are.
-  auto body = [&](Ld &cur, int it) {
-    const bool live = it + kDepth < n_iter;
+  // Half-step pipeline (as in attn_chunk): the next iteration's keys are
+  // loaded once the scores are done, its values once the value MFMAs are.
+  for (int it = 0; it < n_iter; ++it) {
+    const bool live = it + 1 < n_iter;
     const int t0 = start + it * kItTok;
     // --- scores of the four key tiles
     float s2[kKT][NSET];
@@ -1034,15 +1023,17 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
             C = mfma32(AK[st][pt][i], pack_h8(P[4 * i], P[4 * i + 1], P[4 * i + 2], P[4 * i + 3]), C);
         // 2^(qshift - 16) times the folded score (the fp16 scale and zero enter
         // mixed-precision FMAs as stored; the power of two is in the scale)
-        float s = 0.0f;
+        // (two independent chains: no dependent mixed FMAs back to back)
+        float sp[2] = {0.0f, 0.0f};
 #pragma unroll
         for (int gm = 0; gm < NG; ++gm) {
           const half2_t kab = as_h2(cur.kp[q][gm]);
-          s = fmaf((float)kab.x, C[gm], fmaf((float)kab.y, qsl[st][gm], s));
+          sp[gm & 1] = fmaf((float)kab.x, C[gm], fmaf((float)kab.y, qsl[st][gm], sp[gm & 1]));
         }
-        const float v2 = valid ? s * s2scale_q : kNegInf;
+        // -inf for a token past the chunk, as a select (no branch)
+        const float v2 = fmaf(sp[0] + sp[1], s2scale_q, valid ? 0.0f : kNegInf);
         s2[q][st] = v2;
-        if (scores && t0 < end) s_lds[(qs + 4 * st) * max_chunk(G) + (t0 - start) + 16 * q + n] = v2;  // replicas agree
+        if (scores) s_lds[(qs + 4 * st) * max_chunk(G) + (t0 - start) + 16 * q + n] = v2;  // replicas agree
         raise |= __ballot(v2 > m_own[st] + kLazy);
       }
     }
@@ -1097,7 +1088,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    load(cur, it + kDepth, true, false, live);
+    load(cur, it + 1, true, false, live);
     __builtin_amdgcn_sched_barrier(0);
     // --- weights e * alpha into LDS (the A layout of the value MFMAs)
 #pragma unroll
@@ -1113,9 +1104,11 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
         for (int j = 0; j < NGL; ++j) {
           const int gm = (rho + R * j) % NG;
           const half2_t vab = as_h2(cur.vp[q][j]);  // (alpha, beta) of the value group
-          const float w = fmaf(e, (float)vab.x, 0.0f);
           bs_l[st][j] = fmaf(e * dup[j], (float)vab.y, bs_l[st][j]);
-          const _Float16 wh = (_Float16)w, wl = (_Float16)(w - (float)wh);
+          // e * alpha as fp16 high and low parts, each one mixed FMA: the low
+          // part rounds the exact residual e * alpha - high
+          const _Float16 wh = (_Float16)fmaf(e, (float)vab.x, 0.0f);
+          const _Float16 wl = (_Float16)fmaf(e, (float)vab.x, -(float)wh);
           w_lds[w_index(gm, vt, 2 * iq, gv, ei)] = wh;
           w_lds[w_index(gm, vt, 2 * iq + 1, gv, ei)] = wl;
         }
@@ -1143,20 +1136,11 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
       }
     }
     __builtin_amdgcn_sched_barrier(0);
-    load(cur, it + kDepth, false, true, live);
+    load(cur, it + 1, false, true, live);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  };
-  // The bodies run unconditionally (a branch around one would make the
-  // compiler wait for every load in flight at the loop head): an iteration
-  // past the end reads through the empty descriptor and scores -inf, so it
-  // adds nothing.  Chunks of the pool are multiples of kDepth iterations
-  // (make_plan), so only a head's last chunk can run one.
-  for (int it = 0; it < n_iter; it += kDepth) {
-#pragma unroll
-    for (int d = 0; d < kDepth; ++d) body(buf[d], it + d);
   }
 
   // Scores of the chunk: one burst from LDS.
@@ -1645,13 +1629,7 @@ Plan make_plan(const mikv_cache *c, int length) {
   // long_context step); GQA rows carry G queries' work and keep one share
   const int64_t target_hi = group_size_of(c) == 1 ? target * MIKV_CHUNK_HI_SCALE : target;
   p.chunk_hi = std::min(cmax, std::max(128, round_up(target_hi / bh, 128)));
-  // the 2-bit pool under GQA runs on the matrix cores, int2_depth(G)
-  // iterations of kItTok tokens at a time: its chunks are whole multiples
-  // of that too
-  const int G = group_size_of(c);
-  const bool mfma_lo = c->lo_bits == 2 && G >= 2 && c->key_block == 0;
-  const int mult_lo = mfma_lo ? std::lcm(128, kItTok * int2_depth(G)) : 128;
-  p.chunk_lo = std::min(cmax / mult_lo * mult_lo, std::max(mult_lo, round_up(target / bl, mult_lo)));
+  p.chunk_lo = std::min(cmax, std::max(128, round_up(target / bl, 128)));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
   p.nc_lo = evicting(c) ? 0 : std::max(1, (span_lo + p.chunk_lo - 1) / p.chunk_lo);
   // every token is in one of the pools, so at least length - cap_hi are in
