@@ -19,7 +19,12 @@ before the timed region starts.  Prints ONE JSON line on stdout:
   secondary  the same fields for a second workload (default llama2_13b, the
              largest cache by bytes) timed in the same run;
   mall       untimed diagnostic: event-bracketed whole steps with warm caches
-             and with the 256 MB last-level cache flushed before each step.
+             and with the 256 MB last-level cache flushed before each step;
+  read_ceiling  the read bandwidth of a plain streaming kernel over 1 GiB
+             (mikv_stream_read_probe): what HBM gives a plain kernel here;
+             roofline.read_ceiling_same_bytes is the same probe over the
+             step's own byte count and roofline.frac_of_read_ceiling the
+             attention kernel's achieved / that (the practical ceiling).
 
 Only one GPU is used; --gpus above 1 exits with an error.
 """
@@ -182,6 +187,34 @@ def copy_probe(mb: int):
     rec = {"copy_probe_MB": mb, "ms_per_copy": round(ms, 4), "copy_read_plus_write_GBps": round(2 * n / ms / 1e6, 1),
            "ms_per_sum": round(ms_r, 4), "sum_read_GBps": round(n / ms_r / 1e6, 1)}
     print(json.dumps(rec), flush=True)
+
+
+def read_ceiling(mb: int, reps: int = 10):
+    """The library's streaming-read probe (16-byte loads, four in flight per
+    thread, nothing else) over `mb` MiB, timed with HIP events on its stream:
+    the read bandwidth a plain kernel reaches on this device, the practical
+    ceiling of the HBM-bound kernels next to the 8 TB/s data-sheet peak."""
+    import torch
+
+    from paper_2402_18096_amd import mikv
+    n = mb * (1 << 20)
+    buf = torch.empty(n, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for _ in range(3):
+        mikv.mikv_stream_read_probe(buf, sink)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        mikv.mikv_stream_read_probe(buf, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    del buf
+    torch.cuda.empty_cache()
+    return {"kernel": "stream_read_kernel (mikv_stream_read_probe)", "bytes": n, "launches": reps,
+            "mean_launch_us": round(us, 2), "GBps": round(n / us / 1e3, 1)}
 
 
 MFMA_FP16_PEAK_TFLOPS = 2500.0  # dense fp16 matrix-core peak of one MI355X
@@ -375,6 +408,14 @@ def run_workload(wl, args, steps: int, warmup: int, cpu_seconds: float, overridd
         ", ".join(f"{p} {mean(dur[p]) * 1e3:.1f}" for p in phases))
     del dec
     torch.cuda.empty_cache()
+    if roofline and args.read_probe_mb > 0:
+        # the probe over as many bytes as the step reads, re-read the same
+        # way (so the last-level cache keeps the same share of them)
+        ceil_w = read_ceiling(max(1, math.ceil(mean_bytes / (1 << 20))))
+        roofline["read_ceiling_same_bytes"] = ceil_w
+        roofline["frac_of_read_ceiling"] = round(roofline["achieved"] / ceil_w["GBps"], 4)
+        log(f"[bench] {wl.name} streaming-read probe over the same bytes: {ceil_w['GBps']} GB/s; attn_partial at "
+            f"{100 * roofline['frac_of_read_ceiling']:.1f} % of it")
 
     cpu = None
     if cpu_seconds > 0:
@@ -430,6 +471,9 @@ def main():
                          "1 GiB read that evicts the 256 MB last-level cache (cold)")
     ap.add_argument("--prefill-importance", action="store_true",
                     help="instead of the bench: time the prompt-importance kernel on the workload's prompt")
+    ap.add_argument("--read-probe-mb", type=int, default=1024, metavar="MB",
+                    help="size of the streaming-read probe run before the workloads (the measured read "
+                         "ceiling reported next to the data-sheet peak; 0 skips it)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
                     help="instead of the bench: time a plain device-to-device copy of MB megabytes")
     args = ap.parse_args()
@@ -447,6 +491,10 @@ def main():
         return prefill_importance_probe(args.workload, max(1, args.steps if args.steps < 256 else 3))
     wl = apply_overrides(workloads.WORKLOADS[args.workload], args.override)
     cpu_s = 0.0 if args.no_cpu_baseline else args.cpu_seconds
+    ceiling = read_ceiling(args.read_probe_mb) if args.read_probe_mb > 0 else None
+    if ceiling:
+        log(f"[bench] streaming-read probe: {ceiling['GBps']} GB/s over {args.read_probe_mb} MiB "
+            f"({ceiling['mean_launch_us']} us/launch)")
     head = run_workload(wl, args, args.steps, args.warmup, cpu_s, bool(args.override))
     secondary = None
     if args.secondary and args.secondary not in ("none", args.workload):
@@ -469,6 +517,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         **{k: v for k, v in head.items() if k not in ("value", "ms_per_step")},
+        "read_ceiling": ceiling,
         "secondary": secondary,
     }
     if args.override:

@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 20
+    assert len(names) == 21
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -165,3 +165,15 @@ def test_heavy_budget():
     assert L.mikv_heavy_budget(2 ** 31 - 1, 3, 4, 0, 0) == (2 ** 31 - 1) * 3 // 4   # no 32-bit overflow
     assert L.mikv_heavy_budget(10, 1, 0, 0, 0) == -1
     assert L.mikv_heavy_budget(-1, 1, 2, 0, 0) == -1
+
+
+def test_stream_read_probe_validates_on_the_host():
+    """The read-bandwidth probe refuses a NULL, misaligned or ragged buffer
+    before launching anything."""
+    L = mikv.lib()
+    p = ctypes.c_void_p(0x1000)
+    assert L.mikv_stream_read_probe(None, 1024, p, None) == 1
+    assert L.mikv_stream_read_probe(ctypes.c_void_p(0x1008), 1024, p, None) == 1
+    assert L.mikv_stream_read_probe(p, 1000, p, None) == 1
+    assert L.mikv_stream_read_probe(p, 0, p, None) == 1
+    assert b"16-byte" in L.mikv_last_error()
