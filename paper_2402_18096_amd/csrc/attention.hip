@@ -9,7 +9,8 @@
 //
 // One wave per chunk (many small work units keep every CU streaming).
 // Lanes: LPT = 128/CPL lanes per token, each owning CPL contiguous channels
-// (CPL = 32, or 16 for G = 8); a wave covers 64/LPT tokens per tile and
+// (CPL = 32; 16 from four query heads per KV head; 8 for an fp16 importance
+// pool at eight); a wave covers 64/LPT tokens per tile and
 // UNROLL tiles per iteration.  Rows are read through buffer descriptors
 // spanning the head's occupied slots (reads past them return zero and are
 // masked), contiguous across the lanes of a tile.
@@ -185,13 +186,15 @@ __device__ inline int query_shift(float qmax_lane) {
   }
 }
 
-// Sum over the LPT consecutive lanes of a token (LPT = 4 or 8).
+// Sum over the LPT consecutive lanes of a token (LPT = 4, 8 or 16).
 template <int LPT>
 __device__ inline float token_sum(float v) {
   v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, true));
   v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, true));
-  if constexpr (LPT == 8)  // other quad of the half-row
+  if constexpr (LPT >= 8)  // other quad of the half-row
     v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xF, 0xF, true));
+  if constexpr (LPT == 16)  // other half of the row
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x140, 0xF, 0xF, true));
   return v;
 }
 
@@ -202,9 +205,9 @@ __device__ inline float sum_token_lanes(float v) {
   if constexpr (LPT == 4) {
     v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x124, 0xF, 0xF, false));
     v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));
-  } else {
+  } else if constexpr (LPT == 8) {
     v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xF, 0xF, false));
-  }
+  }  // LPT 16: one token per row
   v += __shfl_xor(v, 16, 64);
   v += __shfl_xor(v, 32, 64);
   return v;
@@ -1257,6 +1260,9 @@ template <int HI, int LO, int G, bool SPLITQ, bool KPC = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
+  // an fp16 importance pool with eight query heads per KV head: 8 channels
+  // per lane, which halves the value sums a lane holds (G x CPL registers)
+  constexpr int CPL_HI = HI == 16 && G >= 8 ? 8 : CPL;
   // Block -> (head, chunk): first every head's importance-pool chunks and
   // the retained-pool chunks that cannot be empty (nc_first per head; with
   // pool_major all importance-pool chunks, the longest-running waves of an
@@ -1285,7 +1291,7 @@ void attn_partial_kernel(AttnArgs A) {
   __shared__ float s_lds[G * max_chunk(G)];  // the chunk's scores, [G][max_chunk(G)]
   if (c < A.nc_hi) {
     if (A.hi_pending) append_in_chunk<HI>(A, h, c);
-    attn_chunk<HI, G, CPL, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
+    attn_chunk<HI, G, CPL_HI, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
   } else if constexpr (KPC) {
     attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>(), true>(A, h, c - A.nc_hi, c, false, s_lds);
   } else if constexpr (LO == 2 && G >= 2) {
