@@ -462,9 +462,10 @@ def main():
     ap.add_argument("--events", choices=["partial", "none"], default="partial",
                     help="events inside the timed steps: around the attention partial kernel (default; gives "
                          "the roofline), or none (wall time only)")
-    ap.add_argument("--event-every", type=int, default=8, metavar="K",
+    ap.add_argument("--event-every", type=int, default=7, metavar="K",
                     help="bracket the attention partial kernel with events on every K-th timed step (each event "
-                         "costs a few microseconds of GPU time; default 8)")
+                         "costs a few microseconds of GPU time; default 7: odd, so the sampled steps alternate "
+                         "between the two grid orders that consecutive steps use)")
     ap.add_argument("--mall-steps", type=int, default=16,
                     help="untimed steps after the phase pass, each bracketed by two events: this many with the "
                          "caches as the previous step left them (warm), then this many each preceded by a "
