@@ -23,8 +23,9 @@ before the timed region starts.  Prints ONE JSON line on stdout:
   read_ceiling  the read bandwidth of a plain streaming kernel over 1 GiB
              (mikv_stream_read_probe): what HBM gives a plain kernel here;
              roofline.read_ceiling_same_bytes is the same probe over the
-             step's own byte count and roofline.frac_of_read_ceiling the
-             attention kernel's achieved / that (the practical ceiling).
+             step's own byte count, passes alternating in direction as the
+             steps do, and roofline.frac_of_read_ceiling the attention
+             kernel's achieved / that (the practical ceiling).
 
 Only one GPU is used; --gpus above 1 exits with an error.
 """
@@ -189,11 +190,13 @@ def copy_probe(mb: int):
     print(json.dumps(rec), flush=True)
 
 
-def read_ceiling(mb: int, reps: int = 10):
+def read_ceiling(mb: int, reps: int = 10, alternate: bool = False):
     """The library's streaming-read probe (16-byte loads, four in flight per
     thread, nothing else) over `mb` MiB, timed with HIP events on its stream:
     the read bandwidth a plain kernel reaches on this device, the practical
-    ceiling of the HBM-bound kernels next to the 8 TB/s data-sheet peak."""
+    ceiling of the HBM-bound kernels next to the 8 TB/s data-sheet peak.
+    With `alternate` consecutive passes run in opposite directions, as the
+    decode steps do."""
     import torch
 
     from paper_2402_18096_amd import mikv
@@ -201,19 +204,20 @@ def read_ceiling(mb: int, reps: int = 10):
     buf = torch.empty(n, dtype=torch.uint8, device="cuda")
     buf.fill_(1)
     sink = torch.zeros(1, dtype=torch.int32, device="cuda")
-    for _ in range(3):
-        mikv.mikv_stream_read_probe(buf, sink)
+    for i in range(3):
+        mikv.mikv_stream_read_probe(buf, sink, alternate and i % 2 == 1)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(reps):
-        mikv.mikv_stream_read_probe(buf, sink)
+    for i in range(reps):
+        mikv.mikv_stream_read_probe(buf, sink, alternate and i % 2 == 0)
     e1.record()
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) / reps * 1e3
     del buf
     torch.cuda.empty_cache()
     return {"kernel": "stream_read_kernel (mikv_stream_read_probe)", "bytes": n, "launches": reps,
+            "directions": "alternating" if alternate else "front to back",
             "mean_launch_us": round(us, 2), "GBps": round(n / us / 1e3, 1)}
 
 
@@ -410,8 +414,9 @@ def run_workload(wl, args, steps: int, warmup: int, cpu_seconds: float, overridd
     torch.cuda.empty_cache()
     if roofline and args.read_probe_mb > 0:
         # the probe over as many bytes as the step reads, re-read the same
-        # way (so the last-level cache keeps the same share of them)
-        ceil_w = read_ceiling(max(1, math.ceil(mean_bytes / (1 << 20))))
+        # way: back to back, in alternating directions (so the last-level
+        # cache serves the same share of them)
+        ceil_w = read_ceiling(max(1, math.ceil(mean_bytes / (1 << 20))), alternate=True)
         roofline["read_ceiling_same_bytes"] = ceil_w
         roofline["frac_of_read_ceiling"] = round(roofline["achieved"] / ceil_w["GBps"], 4)
         log(f"[bench] {wl.name} streaming-read probe over the same bytes: {ceil_w['GBps']} GB/s; attn_partial at "
@@ -435,7 +440,7 @@ def run_workload(wl, args, steps: int, warmup: int, cpu_seconds: float, overridd
         "pct_of_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 2),
         "steps_per_s": round(1e3 / ms, 1),
         "packed_bytes_per_step": int(mean_bytes),
-        "phase_us": {p: round(mean(dur[p]) * 1e3, 2) for p in phases},
+        "phase_us": {p: round(mean(dur[p]) * 1e3, 2) for p in phases} if args.phase_steps > 0 else None,
         "roofline": roofline,
         "mall": mall,
         "cpu_baseline": cpu,

@@ -391,16 +391,18 @@ int mikv_decode_step_noalloc(const mikv_cache *c, int32_t length, const uint16_t
 /*
  * Measurement utility (not part of the method): streams `bytes` of device
  * memory from `buf` with 16-byte loads, four in flight per thread, over a
- * grid of up to 8192 blocks of 256 threads, and nothing else.  Timed by the
- * caller, it gives the read bandwidth a plain kernel reaches on the device:
- * the practical ceiling that the decode kernels' roofline figures are read
- * against, next to the data-sheet peak.  `buf` 16-byte aligned, `bytes` a
- * positive multiple of 16; `sink` one device uint32, written only when the
- * XOR fold of every word read equals an internal constant (it keeps the loads
- * alive; callers ignore it).
+ * grid of up to 8192 blocks of 256 threads, and nothing else; front to back,
+ * or back to front when `backwards` is non-zero (alternating the two, as
+ * consecutive decode steps alternate their order, lets the last-level cache
+ * serve the start of each pass).  Timed by the caller, it gives the read
+ * bandwidth a plain kernel reaches on the device: the practical ceiling that
+ * the decode kernels' roofline figures are read against, next to the
+ * data-sheet peak.  `buf` 16-byte aligned, `bytes` a positive multiple of 16;
+ * `sink` one device uint32, written only when the XOR fold of every word read
+ * equals an internal constant (it keeps the loads alive; callers ignore it).
  * Errors: INVALID_ARG.
  */
-int mikv_stream_read_probe(const void *buf, size_t bytes, uint32_t *sink, void *stream);
+int mikv_stream_read_probe(const void *buf, size_t bytes, int32_t backwards, uint32_t *sink, void *stream);
 
 #ifdef __cplusplus
 }

@@ -79,7 +79,7 @@ _SIGS["mikv_decode_step_noalloc"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p,
                                                c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p,
                                                c_void_p])
 
-_SIGS["mikv_stream_read_probe"] = (c_int32, [c_void_p, c_size_t, c_void_p, c_void_p])
+_SIGS["mikv_stream_read_probe"] = (c_int32, [c_void_p, c_size_t, c_int32, c_void_p, c_void_p])
 
 EXPORTS = tuple(_SIGS)
 
@@ -326,14 +326,15 @@ def mikv_select_prefill(scores: torch.Tensor, k_heavy: int, window: int, hi_mask
                                      _stream()), "mikv_select_prefill")
 
 
-def mikv_stream_read_probe(buf: torch.Tensor, sink: torch.Tensor):
+def mikv_stream_read_probe(buf: torch.Tensor, sink: torch.Tensor, backwards: bool = False):
     """Stream the bytes of `buf` (contiguous, 16-byte aligned device tensor)
-    through the library's read-bandwidth probe; `sink` is one int32."""
+    through the library's read-bandwidth probe, front to back or back to
+    front; `sink` is one int32."""
     if not buf.is_contiguous():
         raise MikvError("mikv_stream_read_probe: buf must be contiguous")
     _require(sink, torch.int32, name="sink")
-    _check(lib().mikv_stream_read_probe(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream()),
-           "mikv_stream_read_probe")
+    _check(lib().mikv_stream_read_probe(_ptr(buf), buf.numel() * buf.element_size(), int(bool(backwards)),
+                                        _ptr(sink), _stream()), "mikv_stream_read_probe")
 
 
 def mikv_decode_step(cache: MikvCache, length: int, q, k_new, v_new, out, k_heavy: int, window: int,

@@ -172,8 +172,8 @@ def test_stream_read_probe_validates_on_the_host():
     before launching anything."""
     L = mikv.lib()
     p = ctypes.c_void_p(0x1000)
-    assert L.mikv_stream_read_probe(None, 1024, p, None) == 1
-    assert L.mikv_stream_read_probe(ctypes.c_void_p(0x1008), 1024, p, None) == 1
-    assert L.mikv_stream_read_probe(p, 1000, p, None) == 1
-    assert L.mikv_stream_read_probe(p, 0, p, None) == 1
+    assert L.mikv_stream_read_probe(None, 1024, 0, p, None) == 1
+    assert L.mikv_stream_read_probe(ctypes.c_void_p(0x1008), 1024, 0, p, None) == 1
+    assert L.mikv_stream_read_probe(p, 1000, 1, p, None) == 1
+    assert L.mikv_stream_read_probe(p, 0, 0, p, None) == 1
     assert b"16-byte" in L.mikv_last_error()
