@@ -156,6 +156,23 @@ def test_full_size_sampled_heads(name):
     torch.cuda.empty_cache()
 
 
+def test_full_size_gqa8_sampled_heads():
+    """Eight query heads per KV head (Llama-2-70b's grouping) at the Mistral
+    cache size (16 x 32 query heads over 4 KV heads, 16384 tokens), in the
+    benchmark's launch configuration, the oracle following three heads over
+    four steps (both grid orders)."""
+    _dev()
+    wl = workloads.WORKLOADS["mistral_7b"].with_(kv_heads=4)
+    NH = wl.n_heads
+    print(f"[full-size] G=8: {NH} heads, context {wl.context}, 4 steps", flush=True)
+    run = SampledLockstep(wl, 4, heads=[0, NH // 2 + 1, NH - 1])
+    run.prefill()
+    for t in range(4):
+        run.step(t)
+    del run
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("name", ["mistral_7b", "long_context"])
 def test_full_size_whole_trajectory(name):
     """The GQA and long-context workloads at full size through their whole
