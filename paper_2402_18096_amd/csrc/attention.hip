@@ -90,7 +90,8 @@ struct AttnArgs {
   // non-NULL) and n_hi does not count it until the re-rank writes it.
   AppendArgs app;
   int hi_pending;
-  int pool_major;  // dispatch every importance-pool chunk first (fp16 importance pools)
+  int pool_major;  // dispatch every importance-pool chunk first (fp16 importance pools under GQA)
+  int res_hi, res_lo;  // heads [0, res) of each pool are read plainly, the others streamed
   int order;       // 0: the grid order below; 1: heads reversed; 2: the whole grid reversed
   // per-channel retained keys (key_block 64): (alpha, beta) words
   // [NH, n_kblk, 128] per key block, found through the token's position
@@ -231,6 +232,9 @@ struct Rows {
 };
 
 typedef __amdgpu_buffer_rsrc_t rsrc_t;
+// Cache-policy bits of the cache-row loads: streamed rows are read
+// non-temporally (the nt bit), the rest plainly; see attn_partial_kernel.
+constexpr int kStreamPolicy = 2;
 constexpr int kRsrcFlags = 0x00020000;  // raw (untyped) buffer, gfx9 descriptor word 3
 
 // A buffer resource over `bytes` bytes at `base`: loads at offsets past the
@@ -242,7 +246,9 @@ __device__ inline rsrc_t make_rsrc(const void *base, uint32_t bytes) {
 // Load one token's row segments (this lane's channels) and group params at
 // byte offsets `orow` (rows) and `opar` (params) of the head's pools.
 // WHICH: 1 the key segment and its group parameters, 2 the value's, 3 both.
-template <int BITS, int CPL, int WHICH = 3>
+// PIECE: bytes between the lane's 16-byte pieces of a row; CPOL: the
+// loads' cache-policy bits.
+template <int BITS, int CPL, int WHICH = 3, int PIECE = 16, int CPOL = 0>
 __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, rsrc_t rkp, rsrc_t rvp, uint32_t orow,
                                      uint32_t opar, uint32_t okp) {
   constexpr int KW = Rows<BITS, CPL>::KW;
@@ -251,41 +257,41 @@ __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, r
 #pragma unroll
     for (int i = 0; i < KW / 4; ++i) {
       if constexpr (LK) {
-        auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, orow + 16 * i, 0, 0);
+        auto a = __builtin_amdgcn_raw_buffer_load_b128(rk, orow + PIECE * i, 0, CPOL);
 #pragma unroll
         for (int j = 0; j < 4; ++j) r.k[4 * i + j] = a[j];
       }
       if constexpr (LV) {
-        auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, orow + 16 * i, 0, 0);
+        auto b = __builtin_amdgcn_raw_buffer_load_b128(rv, orow + PIECE * i, 0, CPOL);
 #pragma unroll
         for (int j = 0; j < 4; ++j) r.v[4 * i + j] = b[j];
       }
     }
   } else if constexpr (KW == 3) {
     if constexpr (LK) {
-      auto a = __builtin_amdgcn_raw_buffer_load_b96(rk, orow, 0, 0);
+      auto a = __builtin_amdgcn_raw_buffer_load_b96(rk, orow, 0, CPOL);
       r.k[0] = a[0]; r.k[1] = a[1]; r.k[2] = a[2];
     }
     if constexpr (LV) {
-      auto b = __builtin_amdgcn_raw_buffer_load_b96(rv, orow, 0, 0);
+      auto b = __builtin_amdgcn_raw_buffer_load_b96(rv, orow, 0, CPOL);
       r.v[0] = b[0]; r.v[1] = b[1]; r.v[2] = b[2];
     }
   } else if constexpr (KW == 2) {
     if constexpr (LK) {
-      auto a = __builtin_amdgcn_raw_buffer_load_b64(rk, orow, 0, 0);
+      auto a = __builtin_amdgcn_raw_buffer_load_b64(rk, orow, 0, CPOL);
       r.k[0] = a[0]; r.k[1] = a[1];
     }
     if constexpr (LV) {
-      auto b = __builtin_amdgcn_raw_buffer_load_b64(rv, orow, 0, 0);
+      auto b = __builtin_amdgcn_raw_buffer_load_b64(rv, orow, 0, CPOL);
       r.v[0] = b[0]; r.v[1] = b[1];
     }
   } else {
-    if constexpr (LK) r.k[0] = __builtin_amdgcn_raw_buffer_load_b32(rk, orow, 0, 0);
-    if constexpr (LV) r.v[0] = __builtin_amdgcn_raw_buffer_load_b32(rv, orow, 0, 0);
+    if constexpr (LK) r.k[0] = __builtin_amdgcn_raw_buffer_load_b32(rk, orow, 0, CPOL);
+    if constexpr (LV) r.v[0] = __builtin_amdgcn_raw_buffer_load_b32(rv, orow, 0, CPOL);
   }
   if constexpr (BITS != 16) {
-    if constexpr (LK) r.kp = __builtin_amdgcn_raw_buffer_load_b32(rkp, okp, 0, 0);
-    if constexpr (LV) r.vp = __builtin_amdgcn_raw_buffer_load_b32(rvp, opar, 0, 0);
+    if constexpr (LK) r.kp = __builtin_amdgcn_raw_buffer_load_b32(rkp, okp, 0, CPOL);
+    if constexpr (LV) r.vp = __builtin_amdgcn_raw_buffer_load_b32(rvp, opar, 0, CPOL);
   }
 }
 
@@ -293,7 +299,7 @@ __device__ inline void load_seg_rows(Rows<BITS, CPL> &r, rsrc_t rk, rsrc_t rv, r
 // (Appendix C).  The key's "parameter" word is then its position; a lane
 // keeps q_c * alpha_c (times the code class factor) and sum_c q_c beta_c for
 // the block of its current token and refreshes them when the block changes.
-template <int BITS, int G, int CPL, bool SPLITQ, int UNROLL, int PREFETCH, bool KPC = false>
+template <int BITS, int G, int CPL, bool SPLITQ, int UNROLL, int PREFETCH, bool KPC = false, bool STREAM = false>
 __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, bool is_hi, float *s_lds) {
   using F = Fmt<BITS>;
   constexpr int LPT = kHeadDim / CPL, TPW = 64 / LPT, NP = CPL / 2;
@@ -343,7 +349,16 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   // byte offset of the lane's segment in a row, and the bit shift that
   // aligns it (non-zero only for the 48-bit 3-bit segments of odd lanes)
   constexpr bool kSeg48 = BITS == 3 && CPL == 16;
-  const uint32_t seg_off = kSeg48 ? 4u * (uint32_t)((3 * part) / 2) : (uint32_t)(part * kSeg);
+  // fp16 rows are read spread: piece j of the lane (8 channels, 16 bytes)
+  // holds channels 8 (part + LPT j) .. + 7, so each load of the LPT lanes of
+  // a token covers whole 128-byte lines of its row, which streaming
+  // (non-temporal) loads need to fetch every line once.  Other formats hold
+  // CPL consecutive channels per lane.
+  constexpr bool kSpread = BITS == 16;
+  constexpr int kPiece = kSpread ? 16 * LPT : 16;
+  auto chan8 = [&](int j) { return kSpread ? 8 * (part + LPT * j) : part * CPL + 8 * j; };  // first channel of piece j
+  const uint32_t seg_off =
+      kSeg48 ? 4u * (uint32_t)((3 * part) / 2) : kSpread ? 16u * (uint32_t)part : (uint32_t)(part * kSeg);
   const int seg_shift = kSeg48 && (part & 1) ? 16 : 0;
   auto seg_words = [&](const uint32_t *raw, uint32_t *out) {
     if constexpr (kSeg48) {
@@ -380,7 +395,7 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
     const rsrc_t akp = live ? rkp : r_none, avp = live ? rvp : r_none;
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u)
-      load_seg_rows<BITS, CPL, decltype(which)::value>(r[u], ak, av, akp, avp, orow + (uint32_t)(u * TPW * kRow),
+      load_seg_rows<BITS, CPL, decltype(which)::value, kPiece, STREAM ? kStreamPolicy : 0>(r[u], ak, av, akp, avp, orow + (uint32_t)(u * TPW * kRow),
                                                        opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u,
                                                        KPC ? okp + (uint32_t)(u * TPW) * 4u
                                                            : opar + (uint32_t)(u * TPW) * (uint32_t)ng * 4u);
@@ -406,16 +421,16 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   uint4 qraw[G][CPL / 8];
 #pragma unroll
   for (int i = 0; i < G; ++i) {
-    const uint4 *q4 = reinterpret_cast<const uint4 *>(A.q + (int64_t)(qh0 + i) * kHeadDim + part * CPL);
+    const uint16_t *qrow = A.q + (int64_t)(qh0 + i) * kHeadDim;
 #pragma unroll
-    for (int j = 0; j < CPL / 8; ++j) qraw[i][j] = q4[j];
+    for (int j = 0; j < CPL / 8; ++j) qraw[i][j] = *reinterpret_cast<const uint4 *>(qrow + chan8(j));
   }
   float bal[SPLITQ ? CPL : 1];
   if constexpr (SPLITQ) {
-    const float4 *b4 = reinterpret_cast<const float4 *>(A.balance + (int64_t)h * kHeadDim + part * CPL);
+    const float *brow = A.balance + (int64_t)h * kHeadDim;
 #pragma unroll
     for (int j = 0; j < CPL / 4; ++j) {
-      const float4 v = b4[j];
+      const float4 v = *reinterpret_cast<const float4 *>(brow + chan8(j >> 1) + 4 * (j & 1));
       bal[4 * j] = v.x;
       bal[4 * j + 1] = v.y;
       bal[4 * j + 2] = v.z;
@@ -702,10 +717,10 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
       rec[kRecN] = __builtin_bit_cast(float, n_pool);
     }
     if (tsub == 0) {
-      float4 *r4 = reinterpret_cast<float4 *>(rec + kRecO + part * CPL);
 #pragma unroll
       for (int c = 0; c < CPL / 4; ++c)
-        r4[c] = make_float4(o[i][4 * c], o[i][4 * c + 1], o[i][4 * c + 2], o[i][4 * c + 3]);
+        *reinterpret_cast<float4 *>(rec + kRecO + chan8(c >> 1) + 4 * (c & 1)) =
+            make_float4(o[i][4 * c], o[i][4 * c + 1], o[i][4 * c + 2], o[i][4 * c + 3]);
     }
   }
 }
@@ -779,7 +794,7 @@ __device__ inline int w_index(int gamma, int vt, int row, int g, int e) {
 }
 constexpr int kWLds = 4 * kVT * 16 * 4 * 8;  // halves (4 KiB per value tile)
 
-template <int G, bool SPLITQ, int NG>
+template <int G, bool SPLITQ, int NG, bool STREAM>
 __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chunk, float *s_lds, _Float16 *w_lds) {
   constexpr int QS = G < 4 ? G : 4;    // distinct query slots in one row block
   constexpr int NSET = G > 4 ? 2 : 1;  // query sets (G = 8: queries 0-3 and 4-7)
@@ -787,6 +802,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
   constexpr int NGL = (NG + R - 1) / R;  // value groups each lane weights
   constexpr int NP = SPLITQ ? 2 : 1;   // fp16 parts of the query
   constexpr int GROUP = kHeadDim / NG;
+  constexpr int kCpol = STREAM ? kStreamPolicy : 0;
   const int lane = threadIdx.x & 63, n = lane & 15, a = lane >> 4;
   const int qs = a % QS, rho = a / QS;
   const int b = h / A.kv_heads, kvh = h % A.kv_heads;
@@ -823,34 +839,34 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
     for (int q = 0; q < kKT; ++q) {
       const uint32_t slot = t0 + 16 * q + n;
       if (keys) {
-        auto kc = __builtin_amdgcn_raw_buffer_load_b64(ak, slot * 32u + 8u * a, 0, 0);
+        auto kc = __builtin_amdgcn_raw_buffer_load_b64(ak, slot * 32u + 8u * a, 0, kCpol);
         d.kc[q][0] = kc[0];
         d.kc[q][1] = kc[1];
         if constexpr (NG == 4) {
-          auto kp = __builtin_amdgcn_raw_buffer_load_b128(akp, slot * 16u, 0, 0);
+          auto kp = __builtin_amdgcn_raw_buffer_load_b128(akp, slot * 16u, 0, kCpol);
 #pragma unroll
           for (int j = 0; j < 4; ++j) d.kp[q][j] = kp[j];
         } else if constexpr (NG == 2) {
-          auto kp = __builtin_amdgcn_raw_buffer_load_b64(akp, slot * 8u, 0, 0);
+          auto kp = __builtin_amdgcn_raw_buffer_load_b64(akp, slot * 8u, 0, kCpol);
           d.kp[q][0] = kp[0];
           d.kp[q][1] = kp[1];
         } else {
-          d.kp[q][0] = __builtin_amdgcn_raw_buffer_load_b32(akp, slot * 4u, 0, 0);
+          d.kp[q][0] = __builtin_amdgcn_raw_buffer_load_b32(akp, slot * 4u, 0, kCpol);
         }
       }
       if (vals) {
         if constexpr (R == 1 && NG == 4) {  // every group: the whole row, one load
-          auto vp = __builtin_amdgcn_raw_buffer_load_b128(avp, slot * 16u, 0, 0);
+          auto vp = __builtin_amdgcn_raw_buffer_load_b128(avp, slot * 16u, 0, kCpol);
 #pragma unroll
           for (int j = 0; j < 4; ++j) d.vp[q][j] = vp[j];
         } else if constexpr (R == 1 && NG == 2) {
-          auto vp = __builtin_amdgcn_raw_buffer_load_b64(avp, slot * 8u, 0, 0);
+          auto vp = __builtin_amdgcn_raw_buffer_load_b64(avp, slot * 8u, 0, kCpol);
           d.vp[q][0] = vp[0];
           d.vp[q][1] = vp[1];
         } else {
 #pragma unroll
           for (int j = 0; j < NGL; ++j)
-            d.vp[q][j] = __builtin_amdgcn_raw_buffer_load_b32(avp, (slot * NG + (uint32_t)((rho + R * j) % NG)) * 4u, 0, 0);
+            d.vp[q][j] = __builtin_amdgcn_raw_buffer_load_b32(avp, (slot * NG + (uint32_t)((rho + R * j) % NG)) * 4u, 0, kCpol);
         }
       }
     }
@@ -858,7 +874,7 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #pragma unroll
       for (int vt = 0; vt < kVT; ++vt) {
         const uint32_t tile = (t0 >> 5) + vt;
-        auto vc = __builtin_amdgcn_raw_buffer_load_b128(av, tile * 1024u + 16u * (uint32_t)lane, 0, 0);
+        auto vc = __builtin_amdgcn_raw_buffer_load_b128(av, tile * 1024u + 16u * (uint32_t)lane, 0, kCpol);
 #pragma unroll
         for (int j = 0; j < 4; ++j) d.vc[vt][j] = vc[j];
       }
@@ -1268,9 +1284,15 @@ template <int HI, int LO, int G, bool SPLITQ, bool KPC = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
-  // an fp16 importance pool with eight query heads per KV head: 8 channels
-  // per lane, which halves the value sums a lane holds (G x CPL registers)
+  // An fp16 importance pool with eight query heads per KV head: 8 channels
+  // per lane, which halves the value sums a lane holds (G x CPL registers).
+  // Streamed importance-pool rows: the lanes of a token read whole 128-byte
+  // lines with each load (fp16: 16 channels per lane in two spread pieces;
+  // INT8: 16 channels, one piece), which non-temporal loads need to fetch a
+  // line once; plainly read rows keep the wider lanes, which cost fewer
+  // cross-lane sums per token.
   constexpr int CPL_HI = HI == 16 && G >= 8 ? 8 : CPL;
+  constexpr int CPL_HI_S = HI == 16 && G >= 8 ? 8 : HI == 16 || HI == 8 ? 16 : CPL;
   // Block -> (head, chunk): first every head's importance-pool chunks and
   // the retained-pool chunks that cannot be empty (nc_first per head; with
   // pool_major all importance-pool chunks, the longest-running waves of an
@@ -1302,21 +1324,37 @@ void attn_partial_kernel(AttnArgs A) {
   }
   if (A.order == 1) h = n_heads - 1 - h;
   __shared__ float s_lds[G * max_chunk(G)];  // the chunk's scores, [G][max_chunk(G)]
+  // The rows of the first res_hi / res_lo heads of each pool (as much as the
+  // last-level cache keeps from one step to the next) are read with plain
+  // loads, which that cache allocates; all other rows are streamed with
+  // non-temporal loads, which do not push the resident rows out and read
+  // HBM faster.
   if (c < A.nc_hi) {
     if (A.hi_pending) append_in_chunk<HI>(A, h, c);
-    attn_chunk<HI, G, CPL_HI, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
+    if (h < A.res_hi)
+      attn_chunk<HI, G, CPL_HI, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
+    else
+      attn_chunk<HI, G, CPL_HI_S, SPLITQ, unroll_for<HI>(), prefetch_for<HI>(), false, true>(A, h, c, c, true, s_lds);
   } else if constexpr (KPC) {
     attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>(), true>(A, h, c - A.nc_hi, c, false, s_lds);
   } else if constexpr (LO == 2 && G >= 2) {
     __shared__ __align__(16) _Float16 w_lds[kWLds];  // value-MFMA weights, see w_index
-    if (A.group == 32)
-      attn_chunk_int2<G, SPLITQ, 4>(A, h, c - A.nc_hi, c, s_lds, w_lds);
-    else if (A.group == 64)
-      attn_chunk_int2<G, SPLITQ, 2>(A, h, c - A.nc_hi, c, s_lds, w_lds);
-    else
-      attn_chunk_int2<G, SPLITQ, 1>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+    const bool res = h < A.res_lo;
+    if (A.group == 32) {
+      if (res) attn_chunk_int2<G, SPLITQ, 4, false>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+      else attn_chunk_int2<G, SPLITQ, 4, true>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+    } else if (A.group == 64) {
+      if (res) attn_chunk_int2<G, SPLITQ, 2, false>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+      else attn_chunk_int2<G, SPLITQ, 2, true>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+    } else {
+      if (res) attn_chunk_int2<G, SPLITQ, 1, false>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+      else attn_chunk_int2<G, SPLITQ, 1, true>(A, h, c - A.nc_hi, c, s_lds, w_lds);
+    }
   } else {
-    attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
+    if (h < A.res_lo)
+      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
+    else
+      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>(), false, true>(A, h, c - A.nc_hi, c, false, s_lds);
   }
 }
 
@@ -1626,9 +1664,19 @@ __global__ __launch_bounds__(kBlock) void importance_kernel(float *acc, const fl
 struct Plan {
   int chunk_hi, chunk_lo, nc_hi, nc_lo;
   int nc_first;  // nc_hi + the retained-pool chunks that hold tokens whatever the split
+  int64_t head_bytes_hi, head_bytes_lo;  // packed bytes of one head's occupied span per pool (upper bound)
 };
 
 int round_up(int64_t x, int m) { return (int)(((x + m - 1) / m) * m); }
+
+// Bytes of the cache read with plain loads each step (the rest is streamed):
+// what the 256 MB last-level cache keeps between steps next to the step's
+// other traffic (measured on long_context: 160 MB 98.9, 192 MB 98.2,
+// 224 MB 95.5 us per launch).
+#ifndef MIKV_RESIDENT_MB
+#define MIKV_RESIDENT_MB 224
+#endif
+constexpr int64_t kResidentBytes = (int64_t)MIKV_RESIDENT_MB << 20;
 
 Plan make_plan(const mikv_cache *c, int length) {
   Plan p;
@@ -1637,6 +1685,8 @@ Plan make_plan(const mikv_cache *c, int length) {
   const int span_hi = std::min(length, c->cap_hi), span_lo = evicting(c) ? 0 : std::min(length, c->cap_lo);
   const int64_t bh = token_bytes(c->hi_bits, c->group), bl = token_bytes(evicting(c) ? 2 : c->lo_bits, c->group);
   const int64_t total = NH * (span_hi * bh + span_lo * bl);
+  p.head_bytes_hi = span_hi * bh;
+  p.head_bytes_lo = span_lo * bl;
   // One wave per chunk; up to 64 KiB (MHA) or 96 KiB (GQA) of packed K/V per
   // chunk (many small work units balance the CUs best), at least 16 KiB so
   // the per-chunk merge stays cheap.  Chunks are whole wave iterations (128
@@ -1702,11 +1752,24 @@ AttnArgs make_args(const mikv_cache *c, const Plan &p, const uint16_t *q, const 
   A.nc_first = p.nc_first;
   A.app = AppendArgs{};
   A.hi_pending = 0;
-  // fp16 importance-pool chunks run longest: dispatched first, the tail of
-  // the grid is shorter (measured: long_context -1.8 %, mistral_7b -2.3 % per
-  // step; an INT8 pool gained nothing, llama2_7b lost 1.2 %)
-  A.pool_major = c->hi_bits == 16 ? 1 : 0;
+  // fp16 importance-pool chunks under GQA run longest: dispatched first, the
+  // tail of the grid is shorter (measured: mistral_7b 66.0 -> 64.7 us per
+  // launch).  With one query head per KV head the resident importance-pool
+  // rows (last-level cache) and the streamed retained-pool rows (HBM) are
+  // best read side by side, head by head (long_context 98.2 -> 95.0 us).
+  A.pool_major = c->hi_bits == 16 && group_size_of(c) > 1 ? 1 : 0;
   A.order = 0;
+  // Rows read plainly: up to kResidentBytes of the cache, importance pool
+  // first (it is read by every step whatever the re-rank does), then
+  // retained-pool heads.
+  {
+    const int64_t NH = n_heads_of(c);
+    int64_t budget = kResidentBytes;
+    const int64_t hb = std::max<int64_t>(p.head_bytes_hi, 1), lb = std::max<int64_t>(p.head_bytes_lo, 1);
+    A.res_hi = (int)std::min<int64_t>(NH, budget / hb);
+    budget -= (int64_t)A.res_hi * p.head_bytes_hi;
+    A.res_lo = A.res_hi == NH ? (int)std::min<int64_t>(NH, budget / lb) : 0;
+  }
   A.lo_kb = c->key_block ? (const uint32_t *)c->lo_kb : nullptr;
   A.lo_pos = c->lo_pos;
   A.n_kblk = c->key_block ? key_blocks_of(c) : 0;
