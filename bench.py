@@ -21,11 +21,13 @@ before the timed region starts.  Prints ONE JSON line on stdout:
   mall       untimed diagnostic: event-bracketed whole steps with warm caches
              and with the 256 MB last-level cache flushed before each step;
   read_ceiling  the read bandwidth of a plain streaming kernel over 1 GiB
-             (mikv_stream_read_probe): what HBM gives a plain kernel here;
-             roofline.read_ceiling_same_bytes is the same probe over the
-             step's own byte count, passes alternating in direction as the
-             steps do, and roofline.frac_of_read_ceiling the attention
-             kernel's achieved / that (the practical ceiling).
+             (mikv_stream_read_probe, non-temporal loads): what HBM gives a
+             plain kernel here; roofline.read_ceiling_same_bytes is the same
+             probe over the step's own byte count, with the attention's
+             split of plain (resident) and non-temporal (streamed) loads and
+             passes alternating in direction as the steps do, and
+             roofline.frac_of_read_ceiling the attention kernel's achieved /
+             that (the practical ceiling).
 
 Only one GPU is used; --gpus above 1 exits with an error.
 """
@@ -190,13 +192,14 @@ def copy_probe(mb: int):
     print(json.dumps(rec), flush=True)
 
 
-def read_ceiling(mb: int, reps: int = 10, alternate: bool = False):
+def read_ceiling(mb: int, reps: int = 10, alternate: bool = False, resident: int = 0):
     """The library's streaming-read probe (16-byte loads, four in flight per
     thread, nothing else) over `mb` MiB, timed with HIP events on its stream:
     the read bandwidth a plain kernel reaches on this device, the practical
     ceiling of the HBM-bound kernels next to the 8 TB/s data-sheet peak.
-    With `alternate` consecutive passes run in opposite directions, as the
-    decode steps do."""
+    The leading `resident` bytes are read with plain loads, the rest
+    non-temporally.  With `alternate` consecutive passes run in opposite
+    directions, as the decode steps do."""
     import torch
 
     from paper_2402_18096_amd import mikv
@@ -205,19 +208,19 @@ def read_ceiling(mb: int, reps: int = 10, alternate: bool = False):
     buf.fill_(1)
     sink = torch.zeros(1, dtype=torch.int32, device="cuda")
     for i in range(3):
-        mikv.mikv_stream_read_probe(buf, sink, alternate and i % 2 == 1)
+        mikv.mikv_stream_read_probe(buf, sink, resident, alternate and i % 2 == 1)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for i in range(reps):
-        mikv.mikv_stream_read_probe(buf, sink, alternate and i % 2 == 0)
+        mikv.mikv_stream_read_probe(buf, sink, resident, alternate and i % 2 == 0)
     e1.record()
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) / reps * 1e3
     del buf
     torch.cuda.empty_cache()
     return {"kernel": "stream_read_kernel (mikv_stream_read_probe)", "bytes": n, "launches": reps,
-            "directions": "alternating" if alternate else "front to back",
+            "directions": "alternating" if alternate else "front to back", "resident_bytes": min(resident, n),
             "mean_launch_us": round(us, 2), "GBps": round(n / us / 1e3, 1)}
 
 
@@ -414,9 +417,12 @@ def run_workload(wl, args, steps: int, warmup: int, cpu_seconds: float, overridd
     torch.cuda.empty_cache()
     if roofline and args.read_probe_mb > 0:
         # the probe over as many bytes as the step reads, re-read the same
-        # way: back to back, in alternating directions (so the last-level
-        # cache serves the same share of them)
-        ceil_w = read_ceiling(max(1, math.ceil(mean_bytes / (1 << 20))), alternate=True)
+        # way: back to back, in alternating directions, the attention's
+        # resident share with plain loads and the rest non-temporally (so the
+        # last-level cache serves the same share of them)
+        from paper_2402_18096_amd import mikv
+        ceil_w = read_ceiling(max(1, math.ceil(mean_bytes / (1 << 20))), alternate=True,
+                              resident=mikv.mikv_resident_bytes())
         roofline["read_ceiling_same_bytes"] = ceil_w
         roofline["frac_of_read_ceiling"] = round(roofline["achieved"] / ceil_w["GBps"], 4)
         log(f"[bench] {wl.name} streaming-read probe over the same bytes: {ceil_w['GBps']} GB/s; attn_partial at "

@@ -389,20 +389,36 @@ int mikv_decode_step_noalloc(const mikv_cache *c, int32_t length, const uint16_t
                              void *const *phase_events, void *stream);
 
 /*
- * Measurement utility (not part of the method): streams `bytes` of device
- * memory from `buf` with 16-byte loads, four in flight per thread, over a
- * grid of up to 8192 blocks of 256 threads, and nothing else; front to back,
- * or back to front when `backwards` is non-zero (alternating the two, as
- * consecutive decode steps alternate their order, lets the last-level cache
- * serve the start of each pass).  Timed by the caller, it gives the read
- * bandwidth a plain kernel reaches on the device: the practical ceiling that
- * the decode kernels' roofline figures are read against, next to the
- * data-sheet peak.  `buf` 16-byte aligned, `bytes` a positive multiple of 16;
- * `sink` one device uint32, written only when the XOR fold of every word read
- * equals an internal constant (it keeps the loads alive; callers ignore it).
+ * Measurement utility (not part of the method): reads `bytes` of device
+ * memory from `buf` and nothing else.  Each block of 256 threads reads one
+ * contiguous chunk (at most 8192 chunks) with 16-byte loads, four in flight
+ * per thread; chunks that start inside the leading `resident_bytes` are read
+ * with plain loads, the others with non-temporal loads, as the attention
+ * reads its resident and streamed rows (mikv_resident_bytes).  Chunks are
+ * dispatched front to back, or back to front when `backwards` is non-zero
+ * (alternating the two, as consecutive decode steps alternate their order).
+ * Timed by the caller, it gives the read bandwidth a plain kernel reaches on
+ * the device: with `resident_bytes` 0 over a buffer larger than the 256 MB
+ * last-level cache, HBM's; over a decode step's bytes with the attention's
+ * split, the ceiling that kernel's roofline figures are read against, next to
+ * the data-sheet peak.  `buf` 16-byte aligned, `bytes` a positive multiple
+ * of 16; `sink` one device uint32, written only when the XOR fold of every
+ * word read equals an internal constant (it keeps the loads alive; callers
+ * ignore it).
  * Errors: INVALID_ARG.
  */
-int mikv_stream_read_probe(const void *buf, size_t bytes, int32_t backwards, uint32_t *sink, void *stream);
+int mikv_stream_read_probe(const void *buf, size_t bytes, size_t resident_bytes, int32_t backwards,
+                           uint32_t *sink, void *stream);
+
+/*
+ * Bytes of a cache that the attention partial phase reads with plain loads
+ * each step, importance pool first, then retained-pool heads (whole heads of
+ * a pool, in head order, while they fit); every other row is read with
+ * non-temporal loads.  The plain reads are what the last-level cache keeps
+ * from one decode step to the next; the non-temporal ones do not push them
+ * out.  A build-time constant (224 MiB unless built otherwise).
+ */
+size_t mikv_resident_bytes(void);
 
 #ifdef __cplusplus
 }

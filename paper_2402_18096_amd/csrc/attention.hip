@@ -1669,14 +1669,7 @@ struct Plan {
 
 int round_up(int64_t x, int m) { return (int)(((x + m - 1) / m) * m); }
 
-// Bytes of the cache read with plain loads each step (the rest is streamed):
-// what the 256 MB last-level cache keeps between steps next to the step's
-// other traffic (measured on long_context: 160 MB 98.9, 192 MB 98.2,
-// 224 MB 95.5 us per launch).
-#ifndef MIKV_RESIDENT_MB
-#define MIKV_RESIDENT_MB 224
-#endif
-constexpr int64_t kResidentBytes = (int64_t)MIKV_RESIDENT_MB << 20;
+
 
 Plan make_plan(const mikv_cache *c, int length) {
   Plan p;

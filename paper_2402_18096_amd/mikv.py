@@ -79,7 +79,8 @@ _SIGS["mikv_decode_step_noalloc"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p,
                                                c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32, c_void_p,
                                                c_void_p])
 
-_SIGS["mikv_stream_read_probe"] = (c_int32, [c_void_p, c_size_t, c_int32, c_void_p, c_void_p])
+_SIGS["mikv_stream_read_probe"] = (c_int32, [c_void_p, c_size_t, c_size_t, c_int32, c_void_p, c_void_p])
+_SIGS["mikv_resident_bytes"] = (c_size_t, [])
 
 EXPORTS = tuple(_SIGS)
 
@@ -326,15 +327,24 @@ def mikv_select_prefill(scores: torch.Tensor, k_heavy: int, window: int, hi_mask
                                      _stream()), "mikv_select_prefill")
 
 
-def mikv_stream_read_probe(buf: torch.Tensor, sink: torch.Tensor, backwards: bool = False):
+def mikv_stream_read_probe(buf: torch.Tensor, sink: torch.Tensor, resident_bytes: int = 0, backwards: bool = False):
     """Stream the bytes of `buf` (contiguous, 16-byte aligned device tensor)
-    through the library's read-bandwidth probe, front to back or back to
+    through the library's read-bandwidth probe, the leading `resident_bytes`
+    with plain loads and the rest non-temporally, front to back or back to
     front; `sink` is one int32."""
     if not buf.is_contiguous():
         raise MikvError("mikv_stream_read_probe: buf must be contiguous")
+    if resident_bytes < 0:
+        raise MikvError("mikv_stream_read_probe: resident_bytes must be >= 0")
     _require(sink, torch.int32, name="sink")
-    _check(lib().mikv_stream_read_probe(_ptr(buf), buf.numel() * buf.element_size(), int(bool(backwards)),
-                                        _ptr(sink), _stream()), "mikv_stream_read_probe")
+    _check(lib().mikv_stream_read_probe(_ptr(buf), buf.numel() * buf.element_size(), int(resident_bytes),
+                                        int(bool(backwards)), _ptr(sink), _stream()), "mikv_stream_read_probe")
+
+
+def mikv_resident_bytes() -> int:
+    """Bytes of a cache the attention reads with plain loads each step (the
+    rest it streams non-temporally)."""
+    return int(lib().mikv_resident_bytes())
 
 
 def mikv_decode_step(cache: MikvCache, length: int, q, k_new, v_new, out, k_heavy: int, window: int,

@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 21
+    assert len(names) == 22
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -172,8 +172,14 @@ def test_stream_read_probe_validates_on_the_host():
     before launching anything."""
     L = mikv.lib()
     p = ctypes.c_void_p(0x1000)
-    assert L.mikv_stream_read_probe(None, 1024, 0, p, None) == 1
-    assert L.mikv_stream_read_probe(ctypes.c_void_p(0x1008), 1024, 0, p, None) == 1
-    assert L.mikv_stream_read_probe(p, 1000, 1, p, None) == 1
-    assert L.mikv_stream_read_probe(p, 0, 0, p, None) == 1
+    assert L.mikv_stream_read_probe(None, 1024, 0, 0, p, None) == 1
+    assert L.mikv_stream_read_probe(ctypes.c_void_p(0x1008), 1024, 0, 0, p, None) == 1
+    assert L.mikv_stream_read_probe(p, 1000, 0, 1, p, None) == 1
+    assert L.mikv_stream_read_probe(p, 0, 0, 0, p, None) == 1
     assert b"16-byte" in L.mikv_last_error()
+
+
+def test_resident_budget_fits_the_last_level_cache():
+    """The attention's plainly-read share of a cache is a positive size below
+    the 256 MB last-level cache it is meant to stay in."""
+    assert 0 < mikv.mikv_resident_bytes() < 256 << 20
