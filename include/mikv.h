@@ -414,11 +414,18 @@ int mikv_stream_read_probe(const void *buf, size_t bytes, size_t resident_bytes,
  * Bytes of a cache that the attention partial phase reads with plain loads
  * each step, importance pool first, then retained-pool heads (whole heads of
  * a pool, in head order, while they fit); every other row is read with
- * non-temporal loads.  The plain reads are what the last-level cache keeps
- * from one decode step to the next; the non-temporal ones do not push them
- * out.  A build-time constant (224 MiB unless built otherwise).
+ * non-temporal loads.  The plain reads are what the 256 MB last-level cache
+ * keeps from one decode step to the next; the non-temporal ones do not push
+ * them out.  Default 224 MiB: right for one cache decoded step after step.
+ * A caller that runs several caches per step (one per layer) shares the
+ * last-level cache among them and should give each a part of it, or 0.
+ * The setting is process-wide and takes effect at the next launch; results
+ * do not depend on it (only which loads are plain).  Set it while no
+ * other thread launches decode calls.
+ * mikv_set_resident_bytes errors: INVALID_ARG above 2^62 bytes.
  */
 size_t mikv_resident_bytes(void);
+int mikv_set_resident_bytes(size_t bytes);
 
 #ifdef __cplusplus
 }

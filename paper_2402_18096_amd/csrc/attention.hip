@@ -34,6 +34,7 @@
 // scores; the finalize phase merges the records exactly, turns scores into
 // probabilities and optionally adds them to the importance scores.
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "append_device.h"
@@ -1671,6 +1672,9 @@ int round_up(int64_t x, int m) { return (int)(((x + m - 1) / m) * m); }
 
 
 
+std::atomic<int64_t> g_resident_bytes{kResidentBytes};
+int64_t resident_budget() { return g_resident_bytes.load(std::memory_order_relaxed); }
+
 Plan make_plan(const mikv_cache *c, int length) {
   Plan p;
   const int64_t NH = n_heads_of(c);
@@ -1752,12 +1756,12 @@ AttnArgs make_args(const mikv_cache *c, const Plan &p, const uint16_t *q, const 
   // best read side by side, head by head (long_context 98.2 -> 95.0 us).
   A.pool_major = c->hi_bits == 16 && group_size_of(c) > 1 ? 1 : 0;
   A.order = 0;
-  // Rows read plainly: up to kResidentBytes of the cache, importance pool
-  // first (it is read by every step whatever the re-rank does), then
-  // retained-pool heads.
+  // Rows read plainly: up to resident_budget() bytes of the cache,
+  // importance pool first (it is read by every step whatever the re-rank
+  // does), then retained-pool heads.
   {
     const int64_t NH = n_heads_of(c);
-    int64_t budget = kResidentBytes;
+    int64_t budget = resident_budget();
     const int64_t hb = std::max<int64_t>(p.head_bytes_hi, 1), lb = std::max<int64_t>(p.head_bytes_lo, 1);
     A.res_hi = (int)std::min<int64_t>(NH, budget / hb);
     budget -= (int64_t)A.res_hi * p.head_bytes_hi;
@@ -2009,4 +2013,12 @@ extern "C" int mikv_importance_update(const mikv_cache *c, int32_t length, const
                          c->q_heads, c->kv_heads);
   }
   return check_launch("mikv_importance_update");
+}
+
+extern "C" size_t mikv_resident_bytes(void) { return (size_t)mikv::resident_budget(); }
+
+extern "C" int mikv_set_resident_bytes(size_t bytes) {
+  if (bytes > ((size_t)1 << 62)) return mikv::set_error(MIKV_ERR_INVALID_ARG, "mikv_set_resident_bytes: %zu bytes is out of range", bytes);
+  mikv::g_resident_bytes.store((int64_t)bytes, std::memory_order_relaxed);
+  return MIKV_OK;
 }

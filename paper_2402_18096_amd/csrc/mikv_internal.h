@@ -15,11 +15,11 @@ namespace mikv {
 constexpr int kHeadDim = 128;
 constexpr int kKeyBlock = 64;  // positions per block of per-channel key parameters
 
-// Bytes of the cache the attention reads with plain loads each step (the
-// rest it streams with non-temporal loads): what the 256 MB last-level cache
-// keeps from one step to the next next to the step's other traffic
+// Default bytes of a cache the attention reads with plain loads each step
+// (the rest it streams with non-temporal loads): what the 256 MB last-level
+// cache keeps from one step to the next next to the step's other traffic
 // (measured on long_context: 160 MB 98.9, 192 MB 98.2, 224 MB 95.5 us per
-// attention launch).  The read probe takes the same split.
+// attention launch).  mikv_set_resident_bytes changes it at run time.
 #ifndef MIKV_RESIDENT_MB
 #define MIKV_RESIDENT_MB 224
 #endif

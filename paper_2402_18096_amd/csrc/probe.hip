@@ -73,4 +73,3 @@ extern "C" int mikv_stream_read_probe(const void *buf, size_t bytes, size_t resi
   return check_launch("mikv_stream_read_probe");
 }
 
-extern "C" size_t mikv_resident_bytes(void) { return (size_t)kResidentBytes; }

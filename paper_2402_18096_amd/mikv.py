@@ -81,6 +81,7 @@ _SIGS["mikv_decode_step_noalloc"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p,
 
 _SIGS["mikv_stream_read_probe"] = (c_int32, [c_void_p, c_size_t, c_size_t, c_int32, c_void_p, c_void_p])
 _SIGS["mikv_resident_bytes"] = (c_size_t, [])
+_SIGS["mikv_set_resident_bytes"] = (c_int32, [c_size_t])
 
 EXPORTS = tuple(_SIGS)
 
@@ -345,6 +346,13 @@ def mikv_resident_bytes() -> int:
     """Bytes of a cache the attention reads with plain loads each step (the
     rest it streams non-temporally)."""
     return int(lib().mikv_resident_bytes())
+
+
+def mikv_set_resident_bytes(nbytes: int) -> None:
+    """Set that share (process-wide, from the next launch on)."""
+    if nbytes < 0:
+        raise MikvError("mikv_set_resident_bytes: bytes must be >= 0")
+    _check(lib().mikv_set_resident_bytes(int(nbytes)), "mikv_set_resident_bytes")
 
 
 def mikv_decode_step(cache: MikvCache, length: int, q, k_new, v_new, out, k_heavy: int, window: int,

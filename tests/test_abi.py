@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 22
+    assert len(names) == 23
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -180,6 +180,18 @@ def test_stream_read_probe_validates_on_the_host():
 
 
 def test_resident_budget_fits_the_last_level_cache():
-    """The attention's plainly-read share of a cache is a positive size below
-    the 256 MB last-level cache it is meant to stay in."""
-    assert 0 < mikv.mikv_resident_bytes() < 256 << 20
+    """The attention's plainly-read share of a cache defaults to a positive
+    size below the 256 MB last-level cache it is meant to stay in, and can be
+    set and restored; an out-of-range size is refused."""
+    default = mikv.mikv_resident_bytes()
+    assert 0 < default < 256 << 20
+    try:
+        mikv.mikv_set_resident_bytes(0)
+        assert mikv.mikv_resident_bytes() == 0
+        mikv.mikv_set_resident_bytes(1 << 40)
+        assert mikv.mikv_resident_bytes() == 1 << 40
+        assert mikv.lib().mikv_set_resident_bytes((1 << 62) + 1) == 1
+        assert mikv.mikv_resident_bytes() == 1 << 40
+    finally:
+        mikv.mikv_set_resident_bytes(default)
+    assert mikv.mikv_resident_bytes() == default

@@ -137,6 +137,42 @@ def test_lockstep_decode(name, fused):
         run.step(t)
 
 
+def _pool_head_bytes(wl, cache, length):
+    """Packed bytes of one head's importance and retained pools as the
+    attention sizes its resident share (occupied span at most the capacity)."""
+    def token_bytes(bits):
+        return 2 * 128 * 2 if bits == 16 else 2 * (128 * bits // 8 + 4 * (128 // wl.group))
+    lo_bits = wl.lo_bits or 2
+    return (min(length, cache.cap_hi) * token_bytes(wl.hi_bits),
+            (min(length, cache.cap_lo) * token_bytes(lo_bits)) if wl.lo_bits else 0)
+
+
+@pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
+@pytest.mark.parametrize("share", ["none", "half_hi", "half_lo"])
+def test_lockstep_streamed_rows(name, share):
+    """The attention reads a resident share of the cache with plain loads and
+    streams the rest with non-temporal loads (streamed fp16 and INT8
+    importance rows 16 channels per lane, fp16 in spread pieces).  With
+    nothing resident, with half the heads' importance pools resident, and
+    with every importance pool and half the retained pools resident, the
+    decode step matches the oracle as it does with the default share."""
+    _dev()
+    wl = workloads.small_workload(name, **SMALL[name])
+    steps = 4
+    default = mikv.mikv_resident_bytes()
+    run = Lockstep(wl, steps, fused=True)
+    try:
+        hb, lb = _pool_head_bytes(wl, run.dec.cache, wl.context + steps)
+        nh = wl.n_heads
+        budget = {"none": 0, "half_hi": (nh // 2) * hb, "half_lo": nh * hb + (nh // 2) * lb}[share]
+        mikv.mikv_set_resident_bytes(budget)
+        run.prefill()
+        for t in range(steps):
+            run.step(t)
+    finally:
+        mikv.mikv_set_resident_bytes(default)
+
+
 @pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
 def test_full_size_sampled_heads(name):
     """Every workload at its full size, in the benchmark's launch configuration
