@@ -18,8 +18,10 @@ before the timed region starts.  Prints ONE JSON line on stdout:
   cpu_baseline  the CPU oracle timed on a bounded sample of the same workload;
   secondary  the same fields for a second workload (default llama2_13b, the
              largest cache by bytes) timed in the same run;
-  mall       untimed diagnostic: event-bracketed whole steps with warm caches
-             and with the 256 MB last-level cache flushed before each step;
+  mall       untimed diagnostic: event-bracketed whole steps with warm caches,
+             with the 256 MB last-level cache flushed before each step, and
+             flushed with every row streamed (resident share 0: what a
+             model whose layers share that cache would see);
   read_ceiling  the read bandwidth of a plain streaming kernel over 1 GiB
              (mikv_stream_read_probe, non-temporal loads): what HBM gives a
              plain kernel here; roofline.read_ceiling_same_bytes is the same
@@ -283,7 +285,7 @@ def run_workload(wl, args, steps: int, warmup: int, cpu_seconds: float, overridd
     from paper_2402_18096_amd import mikv, workloads
 
     dev = torch.device("cuda:0")
-    n_total = warmup + steps + args.phase_steps + 2 * args.mall_steps
+    n_total = warmup + steps + args.phase_steps + 3 * args.mall_steps
     t_setup = time.perf_counter()
     dec = mikv.MikvDecoder(wl, max_len=wl.context + n_total, device=dev, fused=bool(args.fused))
     k, v = workloads.prefill_kv(wl, dev)
@@ -349,36 +351,44 @@ def run_workload(wl, args, steps: int, warmup: int, cpu_seconds: float, overridd
 
     # Diagnostics, untimed: whole steps bracketed by events, warm, then cold
     # (the last-level cache and L2 flushed by reading 1 GiB before each
-    # step, outside the bracket; a read leaves no dirty lines behind).
+    # step, outside the bracket; a read leaves no dirty lines behind), then
+    # cold with nothing read plainly (mikv_set_resident_bytes(0): every row
+    # streamed, the setting for a model whose layers share that cache).
     mall = None
     if args.mall_steps > 0:
         flush = torch.zeros(1 << 28, dtype=torch.float32, device=dev)
         mb, ln, nh = [], dec.length, int(dec.cache.n_hi[0].item())
-        for _ in range(2 * args.mall_steps):
+        for _ in range(3 * args.mall_steps):
             ln, n_attn, nh = track_counts(dec, nh, ln)
             mb.append(dec.cache.packed_bytes(ln, n_attn))
         res = {}
         base = warmup + steps + args.phase_steps
-        for j, kind in enumerate(("warm", "cold")):
+        resident = mikv.mikv_resident_bytes()
+        for j, kind in enumerate(("warm", "cold", "cold_streamed")):
             evs = [fresh_events(2) for _ in range(args.mall_steps)]
+            if kind == "cold_streamed":
+                mikv.mikv_set_resident_bytes(0)
             torch.cuda.synchronize()
             for i in range(args.mall_steps):
                 t = base + j * args.mall_steps + i
-                if kind == "cold":
+                if kind != "warm":
                     flush.sum()  # reads only: no dirty lines left to write back
                 evs[i][0].record()
                 dec.step_native(q[t], kn[t], vn[t])
                 evs[i][1].record()
             torch.cuda.synchronize()
+            mikv.mikv_set_resident_bytes(resident)
             us = sorted(e[0].elapsed_time(e[1]) * 1e3 for e in evs)
             nb = mb[j * args.mall_steps:(j + 1) * args.mall_steps]
             res[kind] = {"step_us_median": round(us[len(us) // 2], 2), "step_us_mean": round(sum(us) / len(us), 2),
                          "effective_GBps_median": round(sum(nb) / len(nb) / (us[len(us) // 2] * 1e-6) / 1e9, 1)}
         del flush
         mall = {**res, "steps_each": args.mall_steps, "flush": "1 GiB fp32 read (sum) before each cold step",
+                "cold_streamed": res["cold_streamed"] | {"resident_bytes": 0},
                 "note": "each step bracketed by two events on the stream (adds about empty_event_bracket_us)"}
         log(f"[bench] {wl.name} whole step (event-bracketed): warm median {res['warm']['step_us_median']} us, "
-            f"cold median {res['cold']['step_us_median']} us")
+            f"cold median {res['cold']['step_us_median']} us, cold with every row streamed "
+            f"{res['cold_streamed']['step_us_median']} us")
 
     total_bytes = sum(step_bytes)
     value = total_bytes / elapsed / 1e9
