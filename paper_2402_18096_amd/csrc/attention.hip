@@ -1235,9 +1235,19 @@ __device__ void attn_chunk_int2(const AttnArgs &A, int h, int chunk, int rec_chu
 #ifndef MIKV_UNROLL_INT4
 #define MIKV_UNROLL_INT4 4
 #endif
-template <int BITS>
+// A balanced 2-bit pool (the query in two fp16 parts) takes half the tiles:
+// with eight it needs 171 registers and two waves per SIMD, with four 136 and
+// three (llama2_13b: 266.6-272.1 -> 261.4-264.4 us per launch, step 303.7-307.4
+// -> 299.2-299.8 us; long_context, unbalanced, keeps eight: four measured
+// even).
+#ifndef MIKV_UNROLL_LOWBIT_SPLIT
+#define MIKV_UNROLL_LOWBIT_SPLIT 4
+#endif
+template <int BITS, bool SPLITQ = false>
 constexpr int unroll_for() {
-  return BITS == 4 || BITS == 3 ? MIKV_UNROLL_INT4 : BITS <= 4 ? MIKV_UNROLL_LOWBIT : MIKV_UNROLL_HIGHBIT;
+  return BITS == 4 || BITS == 3 ? MIKV_UNROLL_INT4
+       : BITS <= 4              ? (SPLITQ ? MIKV_UNROLL_LOWBIT_SPLIT : MIKV_UNROLL_LOWBIT)
+                                : MIKV_UNROLL_HIGHBIT;
 }
 template <int BITS>
 constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PREFETCH_HIGHBIT; }
@@ -1354,9 +1364,9 @@ void attn_partial_kernel(AttnArgs A) {
     }
   } else {
     if (h < A.res_lo)
-      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
+      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO, SPLITQ>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
     else
-      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>(), false, true>(A, h, c - A.nc_hi, c, false, s_lds);
+      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO, SPLITQ>(), prefetch_for<LO>(), false, true>(A, h, c - A.nc_hi, c, false, s_lds);
   }
 }
 
