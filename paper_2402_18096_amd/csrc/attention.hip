@@ -8,12 +8,15 @@
 // A block serves all G query heads of the KV group, so GQA loads K/V once.
 //
 // One wave per chunk (many small work units keep every CU streaming).
-// Lanes: LPT = 128/CPL lanes per token, each owning CPL contiguous channels
-// (CPL = 32; 16 from four query heads per KV head; 8 for an fp16 importance
-// pool at eight); a wave covers 64/LPT tokens per tile and
-// UNROLL tiles per iteration.  Rows are read through buffer descriptors
-// spanning the head's occupied slots (reads past them return zero and are
-// masked), contiguous across the lanes of a tile.
+// Lanes: LPT = 128/CPL lanes per token, each owning CPL channels (CPL = 32;
+// 16 from four query heads per KV head and for fp16 importance rows, whose
+// lanes hold two spread 16-byte pieces so a token's lanes read whole
+// 128-byte lines; 8 for an fp16 importance pool at eight); a wave covers
+// 64/LPT tokens per tile and UNROLL tiles per iteration.  Rows are read
+// through buffer descriptors spanning the head's occupied slots (reads past
+// them return zero and are masked), contiguous across the lanes of a tile:
+// plainly for the cache's resident share (kept in the last-level cache from
+// one step to the next), non-temporally for the rest.
 //
 // Inner loop, with every code c in [0, 2^N) of a group with scale alpha and
 // zero beta (Eq. 1, decoded value alpha*c + beta):
@@ -1339,8 +1342,7 @@ void attn_partial_kernel(AttnArgs A) {
   // The rows of the first res_hi / res_lo heads of each pool (as much as the
   // last-level cache keeps from one step to the next) are read with plain
   // loads, which that cache allocates; all other rows are streamed with
-  // non-temporal loads, which do not push the resident rows out and read
-  // HBM faster.
+  // non-temporal loads, which do not push the resident rows out.
   if (c < A.nc_hi) {
     if (A.hi_pending) append_in_chunk<HI>(A, h, c);
     if (h < A.res_hi)
@@ -1681,8 +1683,8 @@ struct Plan {
 
 int round_up(int64_t x, int m) { return (int)(((x + m - 1) / m) * m); }
 
-
-
+// The resident share (mikv_set_resident_bytes): bytes of a cache read with
+// plain loads.
 std::atomic<int64_t> g_resident_bytes{kResidentBytes};
 int64_t resident_budget() { return g_resident_bytes.load(std::memory_order_relaxed); }
 
