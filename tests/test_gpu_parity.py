@@ -626,3 +626,24 @@ def test_fp16_pool_rounding_edge_cases():
     exact = k.reshape(H, n + n1, 128)[..., :16].astype(np.float64) * 0.5
     assert (exact != want[..., :16].view(np.float16).astype(np.float64)).any()   # ties were rounded
     np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("backwards", [False, True])
+def test_stream_read_probe_reads_every_chunk(backwards):
+    """The read probe (a measurement utility) folds every 16-byte word it
+    reads per thread and writes the sink only when a thread's fold hits its
+    sentinel: a buffer of zeros with the sentinel planted at one word makes
+    the sink appear exactly when that word was read.  Planted at the first,
+    a middle and the last word, in the plainly read (resident) part and in
+    the streamed part, over a ragged size, in both chunk orders."""
+    dev = _dev()
+    sentinel = 0x9E3779B9
+    n16 = 3 * 8192 * 1024 // 16 + 37  # about 1500 chunks, the last one ragged
+    for resident in (0, n16 * 8):
+        for word in (0, n16 // 2 + 5, n16 - 1):
+            buf = torch.zeros(n16 * 4, dtype=torch.int32, device=dev)
+            buf[4 * word + 1] = int(np.uint32(sentinel).view(np.int32))
+            sink = torch.zeros(1, dtype=torch.int32, device=dev)
+            mikv.mikv_stream_read_probe(buf, sink, resident, backwards)
+            torch.cuda.synchronize()
+            assert int(sink.item()) & 0xFFFFFFFF == sentinel, (resident, word)
