@@ -1298,16 +1298,21 @@ template <int HI, int LO, int G, bool SPLITQ, bool KPC = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
+  // 4- and 8-bit retained pools at eight query heads per KV head: 8 channels
+  // per lane (a 4- or 8-byte segment), so the lane's G x CPL value sums fit
+  // the registers of two waves per SIMD instead of spilling
+  constexpr int CPL_LO = (LO == 4 || LO == 8) && G >= 8 ? 8 : CPL;
   // fp16 importance pool: 16 channels per lane in two spread pieces, so the
   // lanes of a token read whole 128-byte lines with each load (which
   // non-temporal loads need to fetch a line once, and which read the
   // resident rows faster too: long_context with an evicting cache 38.9 ->
   // 36.2 us per launch); with eight query heads per KV head 8 channels, which
-  // halves the value sums a lane holds (G x CPL registers).  INT8: streamed
-  // rows 16 channels per lane (one piece per line), resident rows the wider
-  // lanes, which cost fewer cross-lane sums per token.
-  constexpr int CPL_HI = HI == 16 ? (G >= 8 ? 8 : 16) : CPL;
-  constexpr int CPL_HI_S = HI == 16 || HI == 8 ? (G >= 8 && HI == 16 ? 8 : 16) : CPL;
+  // halves the value sums a lane holds (G x CPL registers), and so do INT8
+  // and INT4 importance pools at eight.  INT8 below eight: streamed rows 16
+  // channels per lane (one piece per line), resident rows the wider lanes,
+  // which cost fewer cross-lane sums per token.
+  constexpr int CPL_HI = G >= 8 ? 8 : HI == 16 ? 16 : CPL;
+  constexpr int CPL_HI_S = G >= 8 ? 8 : HI == 16 || HI == 8 ? 16 : CPL;
   // Block -> (head, chunk): first every head's importance-pool chunks and
   // the retained-pool chunks that cannot be empty (nc_first per head; with
   // pool_major all importance-pool chunks, the longest-running waves of an
@@ -1366,9 +1371,9 @@ void attn_partial_kernel(AttnArgs A) {
     }
   } else {
     if (h < A.res_lo)
-      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO, SPLITQ>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
+      attn_chunk<LO, G, CPL_LO, SPLITQ, unroll_for<LO, SPLITQ>(), prefetch_for<LO>()>(A, h, c - A.nc_hi, c, false, s_lds);
     else
-      attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO, SPLITQ>(), prefetch_for<LO>(), false, true>(A, h, c - A.nc_hi, c, false, s_lds);
+      attn_chunk<LO, G, CPL_LO, SPLITQ, unroll_for<LO, SPLITQ>(), prefetch_for<LO>(), false, true>(A, h, c - A.nc_hi, c, false, s_lds);
   }
 }
 

@@ -463,6 +463,27 @@ def test_lockstep_int3_retained_cache(name, extra, fused):
         run.step(t)
 
 
+@pytest.mark.parametrize("lo_bits,extra", [
+    (4, dict(q_heads=4, kv_heads=2)),                         # two query heads per KV head
+    (4, {}),                                                  # four (16-channel lanes)
+    (4, dict(batch=1, q_heads=16, kv_heads=2, context=900)),  # eight (8-channel lanes)
+    (8, dict(q_heads=2, kv_heads=2)),                         # one
+    (8, {}),                                                  # four
+    (8, dict(batch=1, q_heads=16, kv_heads=2, context=900)),  # eight (8-channel lanes)
+])
+@pytest.mark.parametrize("fused", [False, True])
+def test_lockstep_int4_int8_retained_cache(lo_bits, extra, fused):
+    """4- and 8-bit retained caches (the wider low precisions of Tables 1-3)
+    at the Mistral shape with one to eight query heads per KV head: prefill,
+    attention, demotion and re-quantization, bit-exact state every step."""
+    _dev()
+    wl = workloads.small_workload("mistral_7b", **{**SMALL["mistral_7b"], **extra}, lo_bits=lo_bits)
+    run = Lockstep(wl, 4, fused=fused)
+    run.prefill()
+    for t in range(4):
+        run.step(t)
+
+
 @pytest.mark.parametrize("name", ["long_context", "mistral_7b"])
 def test_full_size_int3_retained_sampled_heads(name):
     """The INT3 retained cache at the long_context and Mistral (GQA, four
