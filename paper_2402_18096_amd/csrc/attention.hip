@@ -225,12 +225,12 @@ __device__ inline float sum_token_lanes(float v) {
   return v;
 }
 
-// A 3-bit lane segment of 16 channels is 48 bits: two dwords are loaded
-// from the dword that holds its first bit and shifted (seg_shift) so that
-// the segment starts at bit 0.
+// A 3-bit lane segment of 16 (8) channels is 48 (24) bits: two dwords are
+// loaded from the dword that holds its first bit and shifted (seg_shift) so
+// that the segment starts at bit 0.
 template <int BITS, int CPL>
 struct Rows {
-  static constexpr int KW = BITS == 16 ? CPL / 2 : BITS == 3 && CPL == 16 ? 2 : CPL * BITS / 32;  // raw dwords per segment
+  static constexpr int KW = BITS == 16 ? CPL / 2 : BITS == 3 && CPL <= 16 ? 2 : CPL * BITS / 32;  // raw dwords per segment
   uint32_t k[KW], v[KW];
   uint32_t kp, vp;
 };
@@ -351,8 +351,10 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   static_assert(128 % kPerIter == 0 && max_chunk(G) % 128 == 0, "iteration must divide 128 tokens");
   constexpr int kSeg = Rows<BITS, CPL>::KW * 4;  // bytes loaded per lane's row segment
   // byte offset of the lane's segment in a row, and the bit shift that
-  // aligns it (non-zero only for the 48-bit 3-bit segments of odd lanes)
-  constexpr bool kSeg48 = BITS == 3 && CPL == 16;
+  // aligns it (non-zero only for 3-bit segments of 48 or 24 bits, which
+  // start inside a dword)
+  constexpr bool kSeg3 = BITS == 3 && CPL <= 16;
+  constexpr int kSeg3Bytes = 3 * CPL / 8;
   // fp16 rows are read spread: piece j of the lane (8 channels, 16 bytes)
   // holds channels 8 (part + LPT j) .. + 7, so each load of the LPT lanes of
   // a token covers whole 128-byte lines of its row, which streaming
@@ -362,12 +364,12 @@ __device__ void attn_chunk(const AttnArgs &A, int h, int chunk, int rec_chunk, b
   constexpr int kPiece = kSpread ? 16 * LPT : 16;
   auto chan8 = [&](int j) { return kSpread ? 8 * (part + LPT * j) : part * CPL + 8 * j; };  // first channel of piece j
   const uint32_t seg_off =
-      kSeg48 ? 4u * (uint32_t)((3 * part) / 2) : kSpread ? 16u * (uint32_t)part : (uint32_t)(part * kSeg);
-  const int seg_shift = kSeg48 && (part & 1) ? 16 : 0;
+      kSeg3 ? 4u * (uint32_t)((kSeg3Bytes * part) / 4) : kSpread ? 16u * (uint32_t)part : (uint32_t)(part * kSeg);
+  const int seg_shift = kSeg3 ? 8 * ((kSeg3Bytes * part) % 4) : 0;
   auto seg_words = [&](const uint32_t *raw, uint32_t *out) {
-    if constexpr (kSeg48) {
-      out[0] = seg_shift ? __builtin_amdgcn_alignbit(raw[1], raw[0], 16) : raw[0];
-      out[1] = seg_shift ? raw[1] >> 16 : raw[1];
+    if constexpr (kSeg3) {
+      out[0] = __builtin_amdgcn_alignbit(raw[1], raw[0], seg_shift);
+      out[1] = raw[1] >> seg_shift;
     } else {
 #pragma unroll
       for (int i = 0; i < Rows<BITS, CPL>::KW; ++i) out[i] = raw[i];
@@ -1298,10 +1300,10 @@ template <int HI, int LO, int G, bool SPLITQ, bool KPC = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(MIKV_WAVES_PER_EU)))
 void attn_partial_kernel(AttnArgs A) {
   constexpr int CPL = G >= MIKV_NARROW_FROM_G ? 16 : 32;  // channels per lane
-  // 4- and 8-bit retained pools at eight query heads per KV head: 8 channels
-  // per lane (a 4- or 8-byte segment), so the lane's G x CPL value sums fit
-  // the registers of two waves per SIMD instead of spilling
-  constexpr int CPL_LO = (LO == 4 || LO == 8) && G >= 8 ? 8 : CPL;
+  // 3-, 4- and 8-bit retained pools at eight query heads per KV head: 8
+  // channels per lane (a 3-, 4- or 8-byte segment), so the lane's G x CPL
+  // value sums fit the registers of two waves per SIMD instead of spilling
+  constexpr int CPL_LO = (LO == 3 || LO == 4 || LO == 8) && G >= 8 ? 8 : CPL;
   // fp16 importance pool: 16 channels per lane in two spread pieces, so the
   // lanes of a token read whole 128-byte lines with each load (which
   // non-temporal loads need to fetch a line once, and which read the
