@@ -11,7 +11,7 @@
 // Lanes: LPT = 128/CPL lanes per token, each owning CPL channels (CPL = 32;
 // 16 from four query heads per KV head and for fp16 importance rows, whose
 // lanes hold two spread 16-byte pieces so a token's lanes read whole
-// 128-byte lines; 8 for an fp16 importance pool at eight); a wave covers
+// 128-byte lines; 8 at eight query heads per KV head); a wave covers
 // 64/LPT tokens per tile and UNROLL tiles per iteration.  Rows are read
 // through buffer descriptors spanning the head's occupied slots (reads past
 // them return zero and are masked), contiguous across the lanes of a tile:
