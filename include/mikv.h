@@ -277,6 +277,27 @@ int mikv_decode_attention_finalize(const mikv_cache *c, int32_t length, const ui
                                    size_t workspace_bytes, void *stream);
 
 /*
+ * The attention's probabilities by token position (the softmax over the
+ * sequence of Section 3.4 / Fig. 3, as the slot-ordered outputs of
+ * mikv_decode_attention are laid out by the pools' position maps):
+ *   probs[b, i, hi_pos[h, s]] = probs_hi[b, i, s]  for s < n_hi[h],
+ *   probs[b, i, lo_pos[h, s]] = probs_lo[b, i, s]  for s < n_lo[h],
+ * h = b*Hkv + i/G, and 0 for every other position below `length` (tokens
+ * an evicting cache dropped).
+ *   probs_hi, probs_lo  as written by mikv_decode_attention (probs_lo may be
+ *                       NULL only for an evicting cache);
+ *   probs               fp32 [B, Hq, length], written whole.
+ * The slot maps must be those the attention saw: call it after
+ * mikv_decode_attention and before mikv_select_topk moves slots (the fused
+ * mikv_decode_step re-ranks in the same launch, so its outputs cannot be
+ * remapped afterwards).
+ * Errors: INVALID_ARG (NULL pointers, length < 1), CAPACITY (length >
+ * max_len).
+ */
+int mikv_probs_by_position(const mikv_cache *c, int32_t length, const float *probs_hi, const float *probs_lo,
+                           float *probs, void *stream);
+
+/*
  * Importance update (the heavy-hitter accumulated attention policy MiKV
  * adopts, Sections 3.1 and 4.1): for every occupied importance-pool slot s,
  *   hi_acc[h, s] += ((probs_hi[b, hG, s] + probs_hi[b, hG+1, s]) + ...)

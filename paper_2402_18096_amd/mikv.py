@@ -81,6 +81,7 @@ _SIGS["mikv_decode_step_noalloc"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p,
 
 _SIGS["mikv_stream_read_probe"] = (c_int32, [c_void_p, c_size_t, c_size_t, c_int32, c_void_p, c_void_p])
 _SIGS["mikv_resident_bytes"] = (c_size_t, [])
+_SIGS["mikv_probs_by_position"] = (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p])
 _SIGS["mikv_set_resident_bytes"] = (c_int32, [c_size_t])
 
 EXPORTS = tuple(_SIGS)
@@ -340,6 +341,19 @@ def mikv_stream_read_probe(buf: torch.Tensor, sink: torch.Tensor, resident_bytes
     _require(sink, torch.int32, name="sink")
     _check(lib().mikv_stream_read_probe(_ptr(buf), buf.numel() * buf.element_size(), int(resident_bytes),
                                         int(bool(backwards)), _ptr(sink), _stream()), "mikv_stream_read_probe")
+
+
+def mikv_probs_by_position(cache: MikvCache, length: int, probs_hi: torch.Tensor, probs_lo, probs: torch.Tensor):
+    """Scatter the slot-ordered probabilities of both pools into ``probs``
+    fp32 [B, Hq, length] by token position (0 for dropped tokens)."""
+    _require(probs_hi, torch.float32, name="probs_hi")
+    _require(probs, torch.float32, name="probs")
+    if probs_lo is not None:
+        _require(probs_lo, torch.float32, name="probs_lo")
+    if probs.numel() != cache.batch * cache.q_heads * length:
+        raise MikvError("mikv_probs_by_position: probs must hold B * Hq * length floats")
+    _check(lib().mikv_probs_by_position(cache.ref(), length, _ptr(probs_hi), _ptr(probs_lo), _ptr(probs),
+                                        _stream()), "mikv_probs_by_position")
 
 
 def mikv_resident_bytes() -> int:

@@ -184,6 +184,11 @@ class Lockstep:
             snap["p_hi"] = self.dec.probs_hi.clone()
             snap["p_lo"] = self.dec.probs_lo.clone()
             snap["out"] = self.dec.out.cpu().numpy()
+            # the library's own scatter by position, compared below
+            pos = torch.empty(c.batch * c.q_heads * self.dec.length, dtype=torch.float32, device="cuda")
+            mikv.mikv_probs_by_position(c, self.dec.length, self.dec.probs_hi,
+                                        self.dec.probs_lo if c.lo_bits else None, pos)
+            snap["p_pos"] = pos.cpu().numpy()
 
         self.dec.step(self.q[t].cuda(), self.kn[t].cuda(), self.vn[t].cuda(), after_attention=after_attention,
                       emit_heavy=self.dec.cache.cap_hi <= 8192)
@@ -196,6 +201,9 @@ class Lockstep:
         p_gpu = probs_by_position(self.dec.cache, snap["p_hi"], snap["p_lo"], snap["n_hi"], snap["n_lo"],
                                   snap["hi_pos"], snap["lo_pos"], L)
         assert not np.isnan(p_gpu).any(), f"step {t}: a position got no probability"
+        # the scatter moves the same floats: bit-exact
+        np.testing.assert_array_equal(snap["p_pos"].reshape(NH, G, L), p_gpu,
+                                      err_msg=f"step {t}: mikv_probs_by_position")
         np.testing.assert_allclose(p_gpu, p_ref, atol=P_ATOL, rtol=P_RTOL, err_msg=f"step {t}: probabilities")
         # importance update and selection fed with the GPU's probabilities
         self.orc.accumulate(p_gpu)

@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 23
+    assert len(names) == 24
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -177,6 +177,20 @@ def test_stream_read_probe_validates_on_the_host():
     assert L.mikv_stream_read_probe(p, 1000, 0, 1, p, None) == 1
     assert L.mikv_stream_read_probe(p, 0, 0, 0, p, None) == 1
     assert b"16-byte" in L.mikv_last_error()
+
+
+def test_probs_by_position_validates_on_the_host():
+    """The position scatter refuses NULL buffers (a retained pool needs its
+    probabilities), a non-positive length and one beyond max_len before
+    launching anything."""
+    L = mikv.lib()
+    c = _desc()
+    p = ctypes.c_void_p(0x1000)
+    assert L.mikv_probs_by_position(ctypes.byref(c), 4, None, p, p, None) == 1
+    assert L.mikv_probs_by_position(ctypes.byref(c), 4, p, None, p, None) == 1
+    assert L.mikv_probs_by_position(ctypes.byref(c), 4, p, p, None, None) == 1
+    assert L.mikv_probs_by_position(ctypes.byref(c), 0, p, p, p, None) == 1
+    assert L.mikv_probs_by_position(ctypes.byref(c), c.max_len + 1, p, p, p, None) == 3
 
 
 def test_resident_budget_fits_the_last_level_cache():
