@@ -147,6 +147,53 @@ def _pool_head_bytes(wl, cache, length):
             (min(length, cache.cap_lo) * token_bytes(lo_bits)) if wl.lo_bits else 0)
 
 
+@pytest.mark.gpu
+@pytest.mark.parametrize("name,evict", [("long_context", False), ("mistral_7b", False), ("long_context", True)])
+def test_probs_by_position_full_size(name, evict):
+    """mikv_probs_by_position at a full benchmark shape (the largest grids,
+    a ragged last block): every head's row equals the slot-ordered
+    probabilities gathered by position on the host, bit for bit, and each
+    query head's probabilities sum to 1 over the positions (Section 3.4)."""
+    wl = workloads.WORKLOADS[name].with_(lo_bits=0) if evict else workloads.WORKLOADS[name]
+    dev = _dev()
+    dec = mikv.MikvDecoder(wl, max_len=wl.context + 2, device=dev, fused=False)
+    k, v = workloads.prefill_kv(wl, dev)
+    sc = workloads.initial_scores(wl, dev)
+    qp = workloads.prefill_queries(wl, dev) if wl.balanced else None
+    dec.prefill(k, v, sc, qp)
+    del k, v, qp
+    q, kn, vn = workloads.decode_inputs(wl, 2, dev)
+    c = dec.cache
+    G, NH = wl.group_size, wl.n_heads
+    for t in range(2):
+        snap = {}
+
+        def after_attention():
+            L = dec.length
+            pos = torch.empty(c.batch * c.q_heads * L, dtype=torch.float32, device=dev)
+            mikv.mikv_probs_by_position(c, L, dec.probs_hi, dec.probs_lo if c.lo_bits else None, pos)
+            torch.cuda.synchronize()
+            snap["pos"] = pos.cpu().numpy().reshape(NH, G, L)
+            snap["ph"] = dec.probs_hi.cpu().numpy().reshape(NH, G, c.cap_hi)
+            snap["pl"] = dec.probs_lo.cpu().numpy().reshape(NH, G, c.cap_lo)
+            snap["maps"] = [x.cpu().numpy() for x in (c.n_hi, c.n_lo, c.hi_pos, c.lo_pos)]
+
+        dec.step(q[t], kn[t], vn[t], after_attention=after_attention)
+        torch.cuda.synchronize()
+        L = dec.length
+        n_hi, n_lo, hi_pos, lo_pos = snap["maps"]
+        want = np.zeros((NH, G, L), np.float32)
+        for h in range(NH):
+            want[h][:, hi_pos[h, :n_hi[h]]] = snap["ph"][h, :, :n_hi[h]]
+            if c.lo_bits:
+                want[h][:, lo_pos[h, :n_lo[h]]] = snap["pl"][h, :, :n_lo[h]]
+        if c.lo_bits:
+            assert (n_hi + n_lo == L).all(), f"step {t}: the pools do not hold every position"
+        np.testing.assert_array_equal(snap["pos"], want, err_msg=f"{name} step {t}: mikv_probs_by_position")
+        sums = snap["pos"].astype(np.float64).sum(axis=2)
+        np.testing.assert_allclose(sums, 1.0, atol=1e-4, err_msg=f"{name} step {t}: probabilities do not sum to 1")
+
+
 @pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
 @pytest.mark.parametrize("share", ["none", "half_hi", "half_lo"])
 def test_lockstep_streamed_rows(name, share):
