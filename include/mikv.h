@@ -308,6 +308,23 @@ int mikv_probs_by_position(const mikv_cache *c, int32_t length, const float *pro
 int mikv_importance_update(const mikv_cache *c, int32_t length, const float *probs_hi, void *stream);
 
 /*
+ * Importance update over position-indexed rows (the same H2O accumulation,
+ * Sections 3.1 and 4.1, for callers that keep scores by token position):
+ *   acc[b, k, j] += ((probs[b, kG, j] + probs[b, kG+1, j]) + ...)
+ * for j < length, the G = q_heads / kv_heads query heads of KV head k
+ * summed left to right in fp32, then one fp32 add.
+ *   acc    fp32 [batch, kv_heads, max_len] (in/out; positions >= length
+ *          untouched);
+ *   probs  fp32 [batch, q_heads, max_len] (e.g. mikv_probs_by_position's
+ *          output when max_len = length).
+ * length 0 does nothing.  Errors: INVALID_ARG (NULL pointer, a count < 1,
+ * q_heads not a multiple of kv_heads, length < 0), CAPACITY (length >
+ * max_len).
+ */
+int mikv_importance_update_positions(float *acc, const float *probs, int32_t batch, int32_t q_heads,
+                                     int32_t kv_heads, int32_t length, int32_t max_len, void *stream);
+
+/*
  * Re-rank and demote (Fig. 3 right, Section 3.1): per head, the recent
  * window is positions [length - window, length); eligible tokens are the
  * importance-pool tokens outside the window.  The k_heavy eligible tokens

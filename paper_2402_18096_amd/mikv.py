@@ -82,6 +82,8 @@ _SIGS["mikv_decode_step_noalloc"] = (c_int32, [_PC, c_int32, c_void_p, c_void_p,
 _SIGS["mikv_stream_read_probe"] = (c_int32, [c_void_p, c_size_t, c_size_t, c_int32, c_void_p, c_void_p])
 _SIGS["mikv_resident_bytes"] = (c_size_t, [])
 _SIGS["mikv_probs_by_position"] = (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p])
+_SIGS["mikv_importance_update_positions"] = (c_int32, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32,
+                                                       c_int32, c_void_p])
 _SIGS["mikv_set_resident_bytes"] = (c_int32, [c_size_t])
 
 EXPORTS = tuple(_SIGS)
@@ -354,6 +356,18 @@ def mikv_probs_by_position(cache: MikvCache, length: int, probs_hi: torch.Tensor
         raise MikvError("mikv_probs_by_position: probs must hold B * Hq * length floats")
     _check(lib().mikv_probs_by_position(cache.ref(), length, _ptr(probs_hi), _ptr(probs_lo), _ptr(probs),
                                         _stream()), "mikv_probs_by_position")
+
+
+def mikv_importance_update_positions(acc: torch.Tensor, probs: torch.Tensor, length: int):
+    """H2O accumulation over position-indexed rows: acc fp32 [B, Hkv, Lmax]
+    += the group sums of probs fp32 [B, Hq, Lmax] at positions < length."""
+    _require(acc, torch.float32, name="acc")
+    _require(probs, torch.float32, name="probs")
+    if acc.dim() != 3 or probs.dim() != 3 or acc.shape[0] != probs.shape[0] or acc.shape[2] != probs.shape[2]:
+        raise MikvError("mikv_importance_update_positions: acc [B, Hkv, Lmax] and probs [B, Hq, Lmax] expected")
+    B, Hkv, Lmax = acc.shape
+    _check(lib().mikv_importance_update_positions(_ptr(acc), _ptr(probs), B, probs.shape[1], Hkv, length, Lmax,
+                                                  _stream()), "mikv_importance_update_positions")
 
 
 def mikv_resident_bytes() -> int:

@@ -23,7 +23,7 @@ def declared_symbols():
 def test_every_declared_symbol_is_exported():
     L = mikv.lib()
     names = declared_symbols()
-    assert len(names) == 24
+    assert len(names) == 25
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(mikv.EXPORTS)
@@ -191,6 +191,21 @@ def test_probs_by_position_validates_on_the_host():
     assert L.mikv_probs_by_position(ctypes.byref(c), 4, p, p, None, None) == 1
     assert L.mikv_probs_by_position(ctypes.byref(c), 0, p, p, p, None) == 1
     assert L.mikv_probs_by_position(ctypes.byref(c), c.max_len + 1, p, p, p, None) == 3
+
+
+def test_importance_update_positions_validates_on_the_host():
+    """The position-indexed importance update refuses NULL buffers, empty
+    or ungrouped head counts, a negative length and one beyond max_len before
+    launching anything; length 0 is a no-op that touches no memory."""
+    L = mikv.lib()
+    p = ctypes.c_void_p(0x1000)
+    assert L.mikv_importance_update_positions(None, p, 1, 4, 4, 8, 16, None) == 1
+    assert L.mikv_importance_update_positions(p, None, 1, 4, 4, 8, 16, None) == 1
+    assert L.mikv_importance_update_positions(p, p, 0, 4, 4, 8, 16, None) == 1
+    assert L.mikv_importance_update_positions(p, p, 1, 6, 4, 8, 16, None) == 1
+    assert L.mikv_importance_update_positions(p, p, 1, 4, 4, -1, 16, None) == 1
+    assert L.mikv_importance_update_positions(p, p, 1, 4, 4, 17, 16, None) == 3
+    assert L.mikv_importance_update_positions(p, p, 1, 4, 4, 0, 16, None) == 0
 
 
 def test_resident_budget_fits_the_last_level_cache():

@@ -194,6 +194,32 @@ def test_probs_by_position_full_size(name, evict):
         np.testing.assert_allclose(sums, 1.0, atol=1e-4, err_msg=f"{name} step {t}: probabilities do not sum to 1")
 
 
+@pytest.mark.gpu
+@pytest.mark.parametrize("B,Hq,Hkv,L,Lmax", [(1, 1, 1, 1, 1), (2, 4, 4, 300, 333), (1, 8, 2, 257, 257),
+                                             (3, 16, 2, 1000, 1500), (4, 32, 32, 32769, 32769),
+                                             (16, 32, 8, 16385, 16386)])
+def test_importance_update_positions_matches_oracle(B, Hq, Hkv, L, Lmax):
+    """mikv_importance_update_positions against the oracle's H2O accumulation
+    (Sections 3.1, 4.1), bit for bit, at tiny, ragged and full benchmark
+    shapes (long_context, mistral_7b); positions at or past L keep their
+    score."""
+    _dev()
+    G = Hq // Hkv
+    g = torch.Generator().manual_seed(B * 1000003 + Hq * 1009 + L)
+    probs = torch.rand(B, Hq, Lmax, generator=g) * 2e-3
+    acc = torch.rand(B, Hkv, Lmax, generator=g) * 50.0
+    acc_gpu = acc.cuda()
+    mikv.mikv_importance_update_positions(acc_gpu, probs.cuda(), L)
+    torch.cuda.synchronize()
+    got = acc_gpu.cpu().numpy()
+    a, p = acc.numpy(), probs.numpy()
+    want = a.copy()
+    for b in range(B):
+        for k in range(Hkv):
+            want[b, k, :L] = oracle.accumulate(a[b, k, :L], p[b, k * G:(k + 1) * G, :L])
+    np.testing.assert_array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
 @pytest.mark.parametrize("name", workloads.WORKLOAD_ORDER)
 @pytest.mark.parametrize("share", ["none", "half_hi", "half_lo"])
 def test_lockstep_streamed_rows(name, share):
