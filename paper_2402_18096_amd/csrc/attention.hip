@@ -1580,8 +1580,16 @@ void attn_finalize_kernel(AttnArgs A, int accumulate, int tiles_hi, int tiles_lo
 #define MIKV_LO_TILES 8
 #endif
 // Retained-pool probability tiles per finalize block (a tile per query head
-// of the group costs the same registers as kLoTiles tiles of one head).
-__host__ __device__ constexpr int lo_tiles_per_block(int G) { return MIKV_LO_TILES / G > 1 ? MIKV_LO_TILES / G : 1; }
+// of the group costs the same registers as G tiles of one head):
+// MIKV_LO_TILES / G, except 4 at G = 4, where the fewer, longer blocks (216
+// registers, two waves per SIMD) finish the step sooner than 2 or 1 tiles
+// per block (8 is slower again).
+#ifndef MIKV_LO_TILES_G4
+#define MIKV_LO_TILES_G4 4
+#endif
+__host__ __device__ constexpr int lo_tiles_per_block(int G) {
+  return G == 4 ? MIKV_LO_TILES_G4 : MIKV_LO_TILES / G > 1 ? MIKV_LO_TILES / G : 1;
+}
 
 template <int G, int HI, int LO>
 __global__ __launch_bounds__(kBlock) void finalize_select_kernel(AttnArgs A, int tiles_hi, int tiles_lo, SelArgs S) {
