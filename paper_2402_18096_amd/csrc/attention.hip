@@ -1274,6 +1274,9 @@ constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PR
 #ifndef MIKV_CHUNK_HI_SCALE
 #define MIKV_CHUNK_HI_SCALE 2  // MHA importance-pool chunks hold this many times the bytes
 #endif
+#ifndef MIKV_CHUNK_HI_SCALE_F16
+#define MIKV_CHUNK_HI_SCALE_F16 4  // the same for an fp16 importance pool
+#endif
 
 // The decode step's new token: written into importance-pool slot n_hi by
 // the wave whose chunk holds that slot, before the wave reads its chunk (no
@@ -1719,10 +1722,12 @@ Plan make_plan(const mikv_cache *c, int length) {
   const int64_t chunk_kb = group_size_of(c) == 1 ? MIKV_CHUNK_KB_MHA : MIKV_CHUNK_KB;
   int64_t target = std::max<int64_t>(std::min<int64_t>(total / 4096, chunk_kb << 10), 16 << 10);
   const int cmax = max_chunk(group_size_of(c));
-  // MHA importance-pool rows cost the least work per byte: twice the bytes
-  // per chunk there halve the per-wave overhead (measured: 4 % of the
-  // long_context step); GQA rows carry G queries' work and keep one share
-  const int64_t target_hi = group_size_of(c) == 1 ? target * MIKV_CHUNK_HI_SCALE : target;
+  // MHA importance-pool rows cost the least work per byte: more bytes per
+  // chunk there cut the per-wave overhead (twice: 4 % of the long_context
+  // step; four times for an fp16 pool: another 1.3 %, where an INT8 pool lost
+  // 2.6 % at the 13B shape); GQA rows carry G queries' work and keep one share
+  const int64_t hi_scale = c->hi_bits == 16 ? MIKV_CHUNK_HI_SCALE_F16 : MIKV_CHUNK_HI_SCALE;
+  const int64_t target_hi = group_size_of(c) == 1 ? target * hi_scale : target;
   p.chunk_hi = std::min(cmax, std::max(128, round_up(target_hi / bh, 128)));
   p.chunk_lo = std::min(cmax, std::max(128, round_up(target / bl, 128)));
   p.nc_hi = std::max(1, (span_hi + p.chunk_hi - 1) / p.chunk_hi);
