@@ -1254,6 +1254,15 @@ constexpr int unroll_for() {
        : BITS <= 4              ? (SPLITQ ? MIKV_UNROLL_LOWBIT_SPLIT : MIKV_UNROLL_LOWBIT)
                                 : MIKV_UNROLL_HIGHBIT;
 }
+// An fp16 importance pool with one query head per KV head (the least work
+// per byte) keeps four tiles in flight (long_context 106.5-107.0 -> 105.0-
+// 105.5 us per step); under GQA and for INT8 pools four were slower
+// (mistral_7b 87.0 -> 92.8, llama2_7b 44.4 -> 46.0).
+#ifndef MIKV_UNROLL_F16_MHA
+#define MIKV_UNROLL_F16_MHA 4
+#endif
+template <int HI, int G>
+constexpr int unroll_hi() { return HI == 16 && G == 1 ? MIKV_UNROLL_F16_MHA : unroll_for<HI>(); }
 template <int BITS>
 constexpr int prefetch_for() { return BITS <= 4 ? MIKV_PREFETCH_LOWBIT : MIKV_PREFETCH_HIGHBIT; }
 
@@ -1356,9 +1365,9 @@ void attn_partial_kernel(AttnArgs A) {
   if (c < A.nc_hi) {
     if (A.hi_pending) append_in_chunk<HI>(A, h, c);
     if (h < A.res_hi)
-      attn_chunk<HI, G, CPL_HI, SPLITQ, unroll_for<HI>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
+      attn_chunk<HI, G, CPL_HI, SPLITQ, unroll_hi<HI, G>(), prefetch_for<HI>()>(A, h, c, c, true, s_lds);
     else
-      attn_chunk<HI, G, CPL_HI_S, SPLITQ, unroll_for<HI>(), prefetch_for<HI>(), false, true>(A, h, c, c, true, s_lds);
+      attn_chunk<HI, G, CPL_HI_S, SPLITQ, unroll_hi<HI, G>(), prefetch_for<HI>(), false, true>(A, h, c, c, true, s_lds);
   } else if constexpr (KPC) {
     attn_chunk<LO, G, CPL, SPLITQ, unroll_for<LO>(), prefetch_for<LO>(), true>(A, h, c - A.nc_hi, c, false, s_lds);
   } else if constexpr (LO == 2 && G >= 2) {
