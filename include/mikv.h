@@ -457,9 +457,13 @@ int mikv_stream_read_probe(const void *buf, size_t bytes, size_t resident_bytes,
  * them out.  Default 224 MiB: right for one cache decoded step after step.
  * A caller that runs several caches per step (one per layer) shares the
  * last-level cache among them and should give each a part of it, or 0.
- * The setting is process-wide and takes effect at the next launch; results
- * do not depend on it (only which loads are plain).  Set it while no
- * other thread launches decode calls.
+ * The setting is process-wide and takes effect at the next launch.  It
+ * decides which loads are plain, and, when a cache's whole fp16 importance
+ * pool lies inside it with one query head per KV head, that pool is split
+ * into longer chunks (fast from the last-level cache, slower from HBM):
+ * results then differ only in fp32 summation order.  Workspace sizes do not
+ * depend on it.  Set it while no other thread launches decode calls, and
+ * not between the _partial and _finalize calls of one attention.
  * mikv_set_resident_bytes errors: INVALID_ARG above 2^62 bytes.
  */
 size_t mikv_resident_bytes(void);

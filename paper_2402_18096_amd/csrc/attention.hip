@@ -1715,7 +1715,10 @@ int round_up(int64_t x, int m) { return (int)(((x + m - 1) / m) * m); }
 std::atomic<int64_t> g_resident_bytes{kResidentBytes};
 int64_t resident_budget() { return g_resident_bytes.load(std::memory_order_relaxed); }
 
-Plan make_plan(const mikv_cache *c, int length) {
+// size_bound: the plan with the most chunks the resident share can give
+// (workspaces are sized from it, so a workspace stays large enough when the
+// share changes).
+Plan make_plan(const mikv_cache *c, int length, bool size_bound = false) {
   Plan p;
   const int64_t NH = n_heads_of(c);
   // an evicting cache has no retained pool: no chunks for it
@@ -1733,9 +1736,13 @@ Plan make_plan(const mikv_cache *c, int length) {
   const int cmax = max_chunk(group_size_of(c));
   // MHA importance-pool rows cost the least work per byte: more bytes per
   // chunk there cut the per-wave overhead (twice: 4 % of the long_context
-  // step; four times for an fp16 pool: another 1.3 %, where an INT8 pool lost
-  // 2.6 % at the 13B shape); GQA rows carry G queries' work and keep one share
-  const int64_t hi_scale = c->hi_bits == 16 ? MIKV_CHUNK_HI_SCALE_F16 : MIKV_CHUNK_HI_SCALE;
+  // step).  Four times pays only for an fp16 pool read from the last-level
+  // cache (the whole pool within the resident share: long_context warm
+  // 1.3 % faster); streamed from HBM those longer waves were slower (cold
+  // step 130 -> 134 us), and an INT8 pool lost 2.6 % at the 13B shape.
+  // GQA rows carry G queries' work and keep one share.
+  const bool hi_resident = !size_bound && NH * p.head_bytes_hi <= resident_budget();
+  const int64_t hi_scale = c->hi_bits == 16 && hi_resident ? MIKV_CHUNK_HI_SCALE_F16 : MIKV_CHUNK_HI_SCALE;
   const int64_t target_hi = group_size_of(c) == 1 ? target * hi_scale : target;
   p.chunk_hi = std::min(cmax, std::max(128, round_up(target_hi / bh, 128)));
   p.chunk_lo = std::min(cmax, std::max(128, round_up(target / bl, 128)));
@@ -1868,8 +1875,7 @@ int check_attention_args(const mikv_cache *c, int32_t length, const uint16_t *q,
     return set_error(MIKV_ERR_INVALID_ARG, "%s: q and balance must be 16-byte aligned", who);
   if (length < 1) return set_error(MIKV_ERR_INVALID_ARG, "%s: length must be >= 1", who);
   if (length > c->max_len) return set_error(MIKV_ERR_CAPACITY, "%s: length %d > max_len %d", who, length, c->max_len);
-  Plan p = make_plan(c, length);
-  size_t need = workspace_bytes_for(c, p);
+  size_t need = workspace_bytes_for(c, make_plan(c, length, true));
   if (!ws || ws_bytes < need) return set_error(MIKV_ERR_CAPACITY, "%s: workspace too small (%zu < %zu)", who, ws_bytes, need);
   return MIKV_OK;
 }
@@ -1882,7 +1888,7 @@ using namespace mikv;
 
 extern "C" size_t mikv_decode_workspace_size(const mikv_cache *c, int32_t length) {
   if (!c || length < 1 || validate_cache(c)) return 0;
-  return workspace_bytes_for(c, make_plan(c, length));
+  return workspace_bytes_for(c, make_plan(c, length, true));
 }
 
 namespace mikv {
