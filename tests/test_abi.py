@@ -208,6 +208,32 @@ def test_importance_update_positions_validates_on_the_host():
     assert L.mikv_importance_update_positions(p, p, 1, 4, 4, 0, 16, None) == 0
 
 
+@pytest.mark.parametrize("shape", [
+    dict(batch=4, q_heads=32, kv_heads=32, cap_hi=3400, cap_lo=29760, max_len=33024),  # long_context
+    dict(batch=16, q_heads=32, kv_heads=8, cap_hi=1700, cap_lo=14848, max_len=16512),  # mistral_7b
+    dict(),
+])
+def test_workspace_size_does_not_depend_on_the_resident_share(shape):
+    """The chunk split of an fp16 importance pool depends on whether the pool
+    lies inside the resident share, but workspaces are sized from the split
+    with the most chunks: a workspace sized under one share is large enough
+    under any other (the size is the same)."""
+    L = mikv.lib()
+    c = _desc(**shape)
+    length = c.max_len
+    default = mikv.mikv_resident_bytes()
+    try:
+        sizes = []
+        for share in (0, default, 1 << 40):
+            mikv.mikv_set_resident_bytes(share)
+            sizes.append((L.mikv_decode_workspace_size(ctypes.byref(c), length),
+                          L.mikv_decode_step_workspace_size(ctypes.byref(c), length)))
+    finally:
+        mikv.mikv_set_resident_bytes(default)
+    assert sizes[0][0] > 0 and sizes[0][1] > 0
+    assert sizes[0] == sizes[1] == sizes[2]
+
+
 def test_resident_budget_fits_the_last_level_cache():
     """The attention's plainly-read share of a cache defaults to a positive
     size below the 256 MB last-level cache it is meant to stay in, and can be
